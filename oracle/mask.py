@@ -1,0 +1,229 @@
+"""LVSA attention-mask oracle.
+
+TEST INFRASTRUCTURE ONLY.  This module is a plain, slow, obviously-correct
+restatement of the LVSA frame-attention rule (Sec. 2 of the LVSA paper,
+"Training-Free Sparse Attention for Long Video Diffusion") and of the
+frame -> block expansion.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the ``cpu_baseline`` leg of ``bench.py`` may import it.  It shares no code
+with the library under ``paper_2605_31057_amd/`` and imports nothing from it.
+
+Integer arithmetic only, so every result is exact and comparable bit for bit.
+
+Notation follows the paper:
+  T      number of latent frames, frames t = 0..T-1
+  P      tokens (spatial patches) per frame, N = T * P tokens
+  W      local window half-width (Def. 2)
+  C      per-frame attention budget in frames (Sec. 2, budget paragraph)
+  T_per  period of the global anchor frames (Def. 2, budget paragraph)
+  G^s    global anchor frames at denoising step s (Eq. 3)
+  A(t)   frames that query frame t attends to (Def. 1, Def. 2)
+
+Readings where the paper is silent (each is listed in the design notes):
+  * Alg. 1 "side with the most room": room below is l, room above is T-1-h;
+    the strictly larger room wins, equal room extends the low side unless
+    ``tie_high`` is set; a side with no room is never extended.
+  * Eq. 3 is applied literally: frame 0 is an anchor only when Eq. 3 puts it
+    there (always at s = 0 mod T_per, which is Def. 2's fixed G).
+  * Frame -> block: a (query block, key block) pair is kept when some token
+    of the query block and some token of the key block belong to an attended
+    frame pair (any-overlap superset of Eq. 2; equal to it when B divides P).
+  * Blocks are ceil(N / B); the last one may be ragged.
+
+Parity pins: tests/test_oracle_mask.py (hand-worked examples under
+tests/golden/, the invariants the paper states, brute force over tokens).
+"""
+
+WINDOW_BASIC = 0      # Def. 2: clipped window [max(0,t-W), min(T-1,t+W)]
+WINDOW_ADAPTIVE = 1   # Sec. 2 "Overlapping frames": shifted window of 2W+1 frames
+WINDOW_EXPANDED = 2   # Alg. 1: adaptive window grown past overlapping anchors
+
+
+def ceil_div(a, b):
+    """Integer ceiling of a / b for a >= 0, b > 0."""
+    return -(-a // b)
+
+
+def anchor_period(T, C, W, tper=0):
+    """T_per (Sec. 2, budget paragraph): ceil(T / (C - (2W+1))) when C > 2W+1.
+
+    A positive ``tper`` is an explicit override of the derived value.
+    """
+    if tper > 0:
+        return tper
+    if C <= 2 * W + 1:
+        raise ValueError("the derived anchor period needs C > 2W+1")
+    return ceil_div(T, C - (2 * W + 1))
+
+
+def anchors(T, T_per, s, rotate=True):
+    """Global anchor frames as a Python set.
+
+    rotate=False: Def. 2's fixed set {t : t mod T_per == 0}.
+    rotate=True:  Eq. 3, G^s = {(s mod T_per + i*T_per) mod T : i = 0..ceil(T/T_per)-1}.
+    """
+    if not rotate:
+        return {t for t in range(T) if t % T_per == 0}
+    k = ceil_div(T, T_per)
+    return {((s % T_per) + i * T_per) % T for i in range(k)}
+
+
+def basic_window(t, W, T):
+    """Def. 2: w_lo(t) = max(0, t-W), w_hi(t) = min(T-1, t+W)."""
+    return max(0, t - W), min(T - 1, t + W)
+
+
+def adaptive_window(t, W, T):
+    """Sec. 2 "Overlapping frames": the window shifted to keep 2W+1 frames.
+
+    w'_lo(t) = max(0, min(t-W, T-1-2W)),  w'_hi(t) = min(T-1, max(t+W, 2W)).
+    """
+    return max(0, min(t - W, T - 1 - 2 * W)), min(T - 1, max(t + W, 2 * W))
+
+
+def expanded_window(t, G, W, T, tie_high=False):
+    """Alg. 1: expanded window bounds for query frame t.
+
+    Start from the adaptive window; while fewer than
+    target = min(2W+1, T-|G|) of its frames are non-global and the window
+    does not yet cover all frames, extend the side with more room by one
+    frame, counting the new frame when it is not an anchor.
+    Returns (l, h, iterations).
+    """
+    l, h = adaptive_window(t, W, T)
+    target = min(2 * W + 1, T - len(G))
+    nonglobal = sum(1 for f in range(l, h + 1) if f not in G)
+    iterations = 0
+    while nonglobal < target and (l > 0 or h < T - 1):
+        room_lo = l
+        room_hi = (T - 1) - h
+        if room_lo > room_hi or (room_lo == room_hi and not tie_high):
+            l -= 1
+            new_frame = l
+        else:
+            h += 1
+            new_frame = h
+        if new_frame not in G:
+            nonglobal += 1
+        iterations += 1
+    return l, h, iterations
+
+
+def window(t, G, W, T, mode, tie_high=False):
+    """Window bounds (l, h) of query frame t in the given window mode."""
+    if mode == WINDOW_BASIC:
+        return basic_window(t, W, T)
+    if mode == WINDOW_ADAPTIVE:
+        return adaptive_window(t, W, T)
+    if mode == WINDOW_EXPANDED:
+        l, h, _ = expanded_window(t, G, W, T, tie_high)
+        return l, h
+    raise ValueError("unknown window mode")
+
+
+def attended_frames(T, s, C=21, W=6, tper=0, mode=WINDOW_EXPANDED,
+                    rotate=True, tie_high=False):
+    """A(t) = G^s  union  window(t) for every query frame t (Def. 2, Eq. 3).
+
+    Returns (T_per, G, [A(0), ..., A(T-1)]) with each A(t) a Python set.
+    """
+    T_per = anchor_period(T, C, W, tper)
+    G = anchors(T, T_per, s, rotate)
+    A = []
+    for t in range(T):
+        l, h = window(t, G, W, T, mode, tie_high)
+        A.append(set(G) | set(range(l, h + 1)))
+    return T_per, G, A
+
+
+def frame_mask(A, T):
+    """T x T list-of-lists of 0/1: M[t][tau] = 1 iff tau in A(t)."""
+    return [[1 if tau in A[t] else 0 for tau in range(T)] for t in range(T)]
+
+
+def block_keep_bruteforce(A, T, P, B):
+    """Kept (q-block, kv-block) pairs by brute force over token pairs.
+
+    Keep (qb, kb) iff some query token i in qb and some key token j in kb
+    have frame(j) in A(frame(i)).  Cost O(N^2); meant for small N only.
+    Returns a list of rows, each a sorted list of kept kv-block indices.
+    """
+    N = T * P
+    nb = ceil_div(N, B)
+    keep = [[False] * nb for _ in range(nb)]
+    for i in range(N):
+        Ai = A[i // P]
+        qb = i // B
+        for j in range(N):
+            if (j // P) in Ai:
+                keep[qb][j // B] = True
+    return [[kb for kb in range(nb) if keep[qb][kb]] for qb in range(nb)]
+
+
+def block_frames(b, T, P, B):
+    """Frames touched by block b: frame(b*B) .. frame(min((b+1)*B, N) - 1)."""
+    N = T * P
+    first = (b * B) // P
+    last = (min((b + 1) * B, N) - 1) // P
+    return range(first, last + 1)
+
+
+def block_keep(A, T, P, B):
+    """Kept (q-block, kv-block) pairs over frame ranges (same rule, any N).
+
+    Keep (qb, kb) iff some frame t touched by qb and some frame tau touched by
+    kb have tau in A(t).
+    """
+    N = T * P
+    nb = ceil_div(N, B)
+    rows = []
+    for qb in range(nb):
+        attended = set()
+        for t in block_frames(qb, T, P, B):
+            attended |= A[t]
+        row = []
+        for kb in range(nb):
+            if any(tau in attended for tau in block_frames(kb, T, P, B)):
+                row.append(kb)
+        rows.append(row)
+    return rows
+
+
+def block_keep_incidence(A, T, P, B):
+    """The same rule written as incidence products (numpy, fast at any N).
+
+    F[b, t] = 1 iff block b touches frame t;  M[t, tau] = 1 iff tau in A(t).
+    Keep (qb, kb) iff (F M F^T)[qb, kb] > 0, i.e. iff some touched frame pair
+    of the two blocks is attended.
+    """
+    import numpy as np
+    N = T * P
+    nb = ceil_div(N, B)
+    F = np.zeros((nb, T), dtype=np.int64)
+    for b in range(nb):
+        for t in block_frames(b, T, P, B):
+            F[b, t] = 1
+    M = np.array(frame_mask(A, T), dtype=np.int64)
+    K = (F @ M @ F.T) > 0
+    return [[int(kb) for kb in np.nonzero(K[qb])[0]] for qb in range(nb)]
+
+
+def to_csr(rows):
+    """Rows of ascending kv-block indices -> (row_ptr, col_idx) Python lists."""
+    row_ptr = [0]
+    col_idx = []
+    for row in rows:
+        col_idx.extend(row)
+        row_ptr.append(len(col_idx))
+    return row_ptr, col_idx
+
+
+def build_mask(T, P, B, s, C=21, W=6, tper=0, mode=WINDOW_EXPANDED,
+               rotate=True, tie_high=False, layer=0):
+    """The whole LVSA mask for one denoising step: (row_ptr, col_idx).
+
+    ``layer`` is accepted and ignored: the paper's pattern is the same for
+    every layer and head.
+    """
+    del layer
+    _, _, A = attended_frames(T, s, C, W, tper, mode, rotate, tie_high)
+    return to_csr(block_keep_incidence(A, T, P, B))

@@ -1,0 +1,159 @@
+"""Pins for the attention oracle (CPU only).
+
+The oracle is checked against closed forms, scalar brute force written from
+Eq. 1, a library attention routine (torch's scaled_dot_product_attention in
+float64) where the mask is full, and the invariants of softmax attention.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import mask as M
+
+
+def _rand(shape, seed):
+    return np.random.default_rng(seed).standard_normal(shape)
+
+
+def test_scalar_bruteforce_eq1():
+    """Eq. 1 written as scalar loops with math.exp, no max shift."""
+    H, N, d = 2, 7, 5
+    q, k, v = _rand((H, N, d), 1), _rand((H, N, d), 2), _rand((H, N, d), 3)
+    got = OA.dense_attention(q, k, v, dtype=np.float64)
+    for h in range(H):
+        for i in range(N):
+            w = [math.exp(sum(q[h, i, c] * k[h, j, c] for c in range(d)) / math.sqrt(d))
+                 for j in range(N)]
+            z = sum(w)
+            for c in range(d):
+                want = sum(w[j] * v[h, j, c] for j in range(N)) / z
+                assert abs(got[h, i, c] - want) < 1e-12
+
+
+def test_two_key_closed_form():
+    """With two keys the weight of key 0 is the logistic of the logit gap."""
+    d = 16
+    q, k, v = _rand((1, d), 4), _rand((2, d), 5), _rand((2, 3), 6)
+    gap = (q[0] @ k[0] - q[0] @ k[1]) / math.sqrt(d)
+    w0 = 1.0 / (1.0 + math.exp(-gap))
+    want = w0 * v[0] + (1 - w0) * v[1]
+    np.testing.assert_allclose(OA.attend(q, k, v)[0], want, rtol=0, atol=1e-14)
+
+
+def test_matches_library_sdpa_full_mask():
+    """A full mask makes block-sparse attention Eq. 1, which torch's SDPA
+    computes (float64, CPU)."""
+    H, N, d, B = 2, 96, 32, 16
+    q, k, v = _rand((H, N, d), 7), _rand((H, N, d), 8), _rand((H, N, d), 9)
+    nb = N // B
+    row_ptr = [i * nb for i in range(nb + 1)]
+    col_idx = list(range(nb)) * nb
+    got = OA.assemble(OA.block_sparse_attention(q, k, v, row_ptr, col_idx, B,
+                                                dtype=np.float64), H, N, d, B,
+                      dtype=np.float64)
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None],
+        torch.from_numpy(v)[None])[0].numpy()
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(OA.dense_attention(q, k, v, np.float64), want,
+                               rtol=0, atol=1e-12)
+
+
+def test_sparse_matches_library_sdpa_with_bool_mask():
+    """A partial block mask equals SDPA with the expanded boolean token mask."""
+    T, P, B, d = 4, 8, 4, 16
+    N = T * P
+    row_ptr, col_idx = M.build_mask(T, P, B, 1, W=0, tper=2)
+    q, k, v = _rand((1, N, d), 10), _rand((1, N, d), 11), _rand((1, N, d), 12)
+    got = OA.assemble(OA.block_sparse_attention(q, k, v, row_ptr, col_idx, B,
+                                                dtype=np.float64), 1, N, d, B,
+                      dtype=np.float64)
+    allowed = np.zeros((N, N), dtype=bool)
+    for qb in range(N // B):
+        for kb in col_idx[row_ptr[qb]:row_ptr[qb + 1]]:
+            allowed[qb * B:(qb + 1) * B, kb * B:(kb + 1) * B] = True
+    assert not allowed.all()
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None],
+        torch.from_numpy(v)[None], attn_mask=torch.from_numpy(allowed))[0].numpy()
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_constant_values_and_identical_keys():
+    """V constant => O constant; identical keys => O = mean of V."""
+    d = 8
+    q = _rand((5, d), 13)
+    k = _rand((9, d), 14)
+    v = np.full((9, d), 0.375)
+    np.testing.assert_allclose(OA.attend(q, k, v), 0.375, rtol=0, atol=1e-15)
+    kk = np.repeat(_rand((1, d), 15), 9, axis=0)
+    vv = _rand((9, d), 16)
+    np.testing.assert_allclose(OA.attend(q, kk, vv),
+                               np.repeat(vv.mean(0, keepdims=True), 5, 0),
+                               rtol=0, atol=1e-14)
+
+
+def test_key_permutation_invariance_and_weights():
+    d = 8
+    q, k, v = _rand((4, d), 17), _rand((11, d), 18), _rand((11, d), 19)
+    perm = np.random.default_rng(20).permutation(11)
+    np.testing.assert_allclose(OA.attend(q, k[perm], v[perm]), OA.attend(q, k, v),
+                               rtol=0, atol=1e-14)
+    p = OA.softmax_rows((q @ k.T) / math.sqrt(d))
+    np.testing.assert_allclose(p.sum(-1), 1.0, rtol=0, atol=1e-15)
+    assert (p > 0).all()
+
+
+def test_large_logits_are_stable():
+    """Max-shifted softmax: logits far beyond exp's range still give finite
+    weights that match the shift-free formula computed in log space."""
+    q = np.array([[30.0, 0.0]])
+    k = np.array([[30.0, 0.0], [29.0, 0.0], [-30.0, 0.0]])
+    v = np.eye(3)
+    got = OA.attend(q, k, v)[0]
+    s = np.array([900.0, 870.0, -900.0]) / math.sqrt(2)
+    lse = s.max() + math.log(np.exp(s - s.max()).sum())
+    np.testing.assert_allclose(got, np.exp(s - lse), rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("s", [0, 1, 2, 3])
+def test_block_mode_equals_frame_mode_when_block_divides_frame(s):
+    """Eq. 2 token for token equals the block form when B divides P (P13)."""
+    T, P, B, d = 4, 16, 8, 8
+    N = T * P
+    q, k, v = _rand((2, N, d), 21), _rand((2, N, d), 22), _rand((2, N, d), 23)
+    _, _, A = M.attended_frames(T, s, W=0, tper=4)
+    row_ptr, col_idx = M.build_mask(T, P, B, s, W=0, tper=4)
+    blk = OA.assemble(OA.block_sparse_attention(q, k, v, row_ptr, col_idx, B,
+                                                dtype=np.float64), 2, N, d, B,
+                      dtype=np.float64)
+    frm = OA.frame_sparse_attention(q, k, v, A, P, dtype=np.float64)
+    np.testing.assert_allclose(blk, frm, rtol=0, atol=1e-13)
+
+
+def test_ragged_last_block_keys_clipped():
+    """Keys of the last, partial block stop at N (no phantom keys)."""
+    keys = OA.block_keys([0, 2], 4, 10)
+    assert keys.tolist() == [0, 1, 2, 3, 8, 9]
+    N, d, B = 10, 4, 4
+    q, k, v = _rand((1, N, d), 24), _rand((1, N, d), 25), _rand((1, N, d), 26)
+    nb = 3
+    out = OA.block_sparse_attention(q, k, v, [0, 3, 6, 9], [0, 1, 2] * 3, B,
+                                    dtype=np.float64)
+    assert out[(0, 2)].shape == (2, d)
+    dense = OA.dense_attention(q, k, v, np.float64)
+    np.testing.assert_allclose(OA.assemble(out, 1, N, d, B, np.float64), dense,
+                               rtol=0, atol=1e-13)
+    assert nb == len([0, 3, 6, 9]) - 1
+
+
+def test_float32_close_to_float64():
+    H, N, d = 1, 256, 128
+    q, k, v = _rand((H, N, d), 27), _rand((H, N, d), 28), _rand((H, N, d), 29)
+    a = OA.dense_attention(q, k, v, np.float32)
+    b = OA.dense_attention(q, k, v, np.float64)
+    assert a.dtype == np.float32
+    assert np.abs(a - b).max() < 1e-5
