@@ -1,0 +1,271 @@
+"""Benchmark of the LVSA hot path on one MI355X.
+
+One step = one denoising step of the hot path on one attention layer:
+the device mask builder rebuilds the block CSR for step s (Eq. 3 anchors,
+Alg. 1 windows, block expansion) and the block-sparse attention kernel runs
+over it, on synthetic bf16 Q/K/V of the Wan2.1-1.3B 6x-horizon layer shape
+(12 heads, 121 latent frames x 30x52 tokens, head_dim 128, block 128,
+C = 21, W = 6).  Successive steps sweep s = 0, 1, 2, ... so the anchors
+rotate as in a denoising loop.  Inputs are resident in HBM before timing.
+
+Prints ONE JSON line.  Besides the step throughput it reports the attention
+call alone (hipEvents), the dense kernel of the same design, the roofline
+position of the sparse kernel, and the CPU oracle on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload wan13_6x]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = ("ms/attention call + effective TFLOP/s (kept blocks) and speedup vs "
+          "dense, Wan-1.3B 6×")
+ATTN_SRC = os.path.join(ROOT, "paper_2605_31057_amd", "csrc", "attention.hip")
+PMC_FILE = os.path.join(ROOT, "profiles", "attn_sparse_wan13_6x_pmc.json")
+
+
+def kept_flops(row_ptr, col_idx, n_tokens, block, heads, d=128):
+    """4*d FLOP per (query, key) pair of real tokens over the kept blocks."""
+    import numpy as np
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    ci = np.asarray(col_idx, dtype=np.int64)
+    nb = len(rp) - 1
+    rows = np.minimum(block, n_tokens - np.arange(nb) * block)
+    cols = np.minimum(block, n_tokens - ci * block)
+    per_row = np.add.reduceat(cols, rp[:-1]) if len(ci) else np.zeros(nb)
+    per_row = np.where(np.diff(rp) > 0, per_row, 0)
+    return 4.0 * d * heads * float((rows * per_row).sum())
+
+
+def median(xs):
+    xs = sorted(xs)
+    return xs[len(xs) // 2]
+
+
+def time_calls(fn, n, warm):
+    import torch
+    for _ in range(warm):
+        fn()
+    evs = []
+    for _ in range(n):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
+
+
+def traffic_from_profile():
+    """HBM bytes per sparse launch from the committed PMC summary, if it was
+    taken on the current kernel source (else None)."""
+    if not os.path.exists(PMC_FILE):
+        return None
+    with open(PMC_FILE) as f:
+        rec = json.load(f)
+    src = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+    if rec.get("attention_src_sha256") != src:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, target_s):
+    """The oracle (numpy fp32, host cores) on sampled query blocks of head 0
+    of the same workload at step 10, scaled to TFLOP/s on kept blocks."""
+    import numpy as np
+    from paper_2605_31057_amd.inputs import make_qkv
+    from oracle import attention as OA
+    from oracle import mask as M
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    t0 = time.perf_counter()
+    rp, ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, 10,
+                          C=w.budget_frames, W=w.window, tper=w.tper)
+    mask_s = time.perf_counter() - t0
+    q, k, v = make_qkv(1, w.n_tokens, value_scale=w.value_scale)
+    q, k, v = (x.float().numpy() for x in (q, k, v))
+    rng = np.random.default_rng(0)
+    order = rng.permutation(len(rp) - 1)
+    done = []
+    t0 = time.perf_counter()
+    for qb in order:
+        OA.block_sparse_attention(q, k, v, rp, ci, w.block, q_blocks=[int(qb)])
+        done.append(int(qb))
+        if time.perf_counter() - t0 >= target_s:
+            break
+    elapsed = time.perf_counter() - t0
+    n = w.n_tokens
+    flops = 0.0
+    for qb in done:
+        rows = min(w.block, n - qb * w.block)
+        cols = sum(min(w.block, n - kb * w.block) for kb in ci[rp[qb]:rp[qb + 1]])
+        flops += 4.0 * 128 * rows * cols
+    return {
+        "value": flops / elapsed / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"{len(done)} query blocks of head 0 (step 10, fp32 numpy "
+                   f"masked softmax), {elapsed:.1f} s; oracle mask build "
+                   f"{mask_s * 1e3:.0f} ms"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="wan13_6x")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path is a single-GPU kernel; see the sharding notes in "
+              "the design document).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2605_31057_amd as L
+    from paper_2605_31057_amd.inputs import WORKLOADS, workload_qkv
+
+    w = WORKLOADS[args.workload]
+    params = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    print(f"[bench] {w.name}: generating inputs", file=sys.stderr, flush=True)
+    q, k, v = (x.cuda() for x in workload_qkv(w))
+    out = torch.empty_like(q)
+    nb = w.n_blocks
+    rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+    ci = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    # Kept FLOP of every step s (host builder, outside the timed region).
+    n_sweep = len(w.steps)
+    flops_of, nnz_of, host_us = {}, {}, []
+    for s in w.steps:
+        t0 = time.perf_counter()
+        csr = L.build_mask(w.frames, w.tokens_per_frame, w.block, s, params)
+        host_us.append((time.perf_counter() - t0) * 1e6)
+        hrp, hci = csr.arrays()
+        flops_of[s] = kept_flops(hrp, hci, w.n_tokens, w.block, w.heads)
+        nnz_of[s] = int(hrp[-1])
+        csr.free()
+    dense_flops = kept_flops(np.arange(nb + 1) * nb, np.tile(np.arange(nb), nb),
+                             w.n_tokens, w.block, w.heads)
+
+    def step(i):
+        s = w.steps[i % n_sweep]
+        m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s, rp, ci,
+                                params=params, stream=stream)
+        L.attention(q, k, v, m, out=out, stream=stream)
+        return s
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    print("[bench] timed steps", file=sys.stderr, flush=True)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    total_flops = 0.0
+    for i in range(args.steps):
+        s = step(args.warmup + i)
+        total_flops += flops_of[s]
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    value = total_flops / args.steps / (ms_step * 1e-3) / 1e12
+
+    # Attention call alone at step 10 and the device mask build alone.
+    s_ref = 10 if 10 in flops_of else w.steps[0]
+    m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
+                            params=params, stream=stream)
+    attn_ms = time_calls(lambda: L.attention(q, k, v, m, out=out, stream=stream),
+                         20, 3)
+    attn_med = median(attn_ms)
+    mask_ms = time_calls(lambda: L.build_mask_device(
+        w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci, params=params,
+        stream=stream), 20, 3)
+    print(f"[bench] attention {attn_med:.3f} ms", file=sys.stderr, flush=True)
+
+    dense = {}
+    if not args.no_dense:
+        print("[bench] dense", file=sys.stderr, flush=True)
+        d_ms = median(time_calls(lambda: L.dense_attention(q, k, v, block=w.block,
+                                                           out=out, stream=stream), 5, 1))
+        dense = {
+            "dense_ms_per_call": d_ms,
+            "dense_tflops": dense_flops / (d_ms * 1e-3) / 1e12,
+            "speedup_vs_dense": d_ms / attn_med,
+            "inv_density": dense_flops / flops_of[s_ref],
+        }
+
+    achieved = flops_of[s_ref] / (attn_med * 1e-3) / 1e12
+    traffic = traffic_from_profile()
+    rec = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "desc": w.desc,
+            "heads": w.heads,
+            "n_tokens": w.n_tokens,
+            "head_dim": 128,
+            "block": w.block,
+            "mask": {"C": w.budget_frames, "W": w.window, "window": "expanded",
+                     "rotate": True, "steps_swept": f"{w.steps[0]}..{w.steps[-1]}"},
+            "parallelism": "single GPU",
+        },
+        "ms_per_attention_call": attn_med,
+        "attention_tflops_kept": achieved,
+        "mask_build_device_us": median(mask_ms) * 1e3,
+        "mask_build_host_us": median(host_us),
+        "nnz_step10": nnz_of[s_ref],
+        "block_density_step10": nnz_of[s_ref] / (nb * nb),
+        **dense,
+        "roofline": {
+            "kernel": "attn_fwd_kernel<128, sparse>",
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

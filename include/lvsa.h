@@ -1,0 +1,212 @@
+/*
+ * lvsa.h -- C ABI of the LVSA block-sparse video attention library (gfx950).
+ *
+ * LVSA ("Training-Free Sparse Attention for Long Video Diffusion") restricts
+ * the self-attention of a video diffusion transformer, taken over the N = T*P
+ * tokens of T latent frames with P spatial tokens each, to a per-query-frame
+ * set of attended frames A(t) (Sec. 2, Def. 1 and Eq. 2).  LVSA's A(t) is the
+ * union of periodic global anchor frames, rotated with the denoising step
+ * (Def. 2, Eq. 3), and a local window of frames around t, shifted and expanded
+ * so every frame attends to the same number of frames (Sec. 2 "Overlapping
+ * frames", Alg. 1).
+ *
+ * The library has two halves:
+ *   - mask builders that turn (T, P, block, step, params) into per-query-block
+ *     lists of kept key blocks (a block CSR), on the host (lvsa_build_mask)
+ *     or on the device (lvsa_build_mask_device);
+ *   - a block-sparse flash-attention forward pass that visits only the kept
+ *     blocks (lvsa_attention), and a dense pass of the same design over every
+ *     block (lvsa_dense_attention, Eq. 1) used as the speed baseline.
+ *
+ * Conventions for every call:
+ *   - Every function returns an lvsa_status (int32_t).  No C++ exception
+ *     crosses this boundary.  Arguments are checked before anything is
+ *     launched; on an error nothing is launched and no output is written.
+ *   - Device pointers are HIP device addresses on the current device.
+ *     Streams are hipStream_t passed as void* (NULL = the default stream).
+ *   - Calls that launch work are asynchronous on the given stream; launch
+ *     failures are reported as LVSA_EDEVICE.
+ *   - All sizes are in elements unless stated otherwise.
+ */
+#ifndef LVSA_H
+#define LVSA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status ---- */
+
+typedef int32_t lvsa_status;
+#define LVSA_OK 0
+#define LVSA_EINVAL (-1)        /* an argument is out of range or inconsistent */
+#define LVSA_ENOMEM (-2)        /* host or device allocation failed            */
+#define LVSA_EDEVICE (-3)       /* a HIP runtime call or kernel launch failed  */
+#define LVSA_EUNSUPPORTED (-4)  /* valid, but not a shape/layout this build has */
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* lvsa_status_str(lvsa_status s);
+
+/* Library ABI version (major*10000 + minor*100 + patch). */
+int32_t lvsa_version(void);
+
+/* ------------------------------------------------------- mask params ---- */
+
+/* Window rules (Sec. 2):
+ *   BASIC     Def. 2: [max(0,t-W), min(T-1,t+W)], clipped at the sequence ends.
+ *   ADAPTIVE  the "Overlapping frames" paragraph: the window shifted to keep
+ *             2W+1 frames, [max(0,min(t-W,T-1-2W)), min(T-1,max(t+W,2W))].
+ *   EXPANDED  Alg. 1: the adaptive window grown one frame at a time on the
+ *             side with more room (room below = l, above = T-1-h) until it
+ *             holds min(2W+1, T-|G|) non-anchor frames.  Default. */
+#define LVSA_WINDOW_BASIC 0
+#define LVSA_WINDOW_ADAPTIVE 1
+#define LVSA_WINDOW_EXPANDED 2
+
+typedef struct lvsa_params {
+  int32_t budget_frames; /* C, per-frame budget in frames (Sec. 2, budget
+                            paragraph).  Used only when tper == 0, and then
+                            must exceed 2W+1.                               */
+  int32_t window;        /* W >= 0, window half-width (Def. 2).              */
+  int32_t tper;          /* T_per: 0 derives ceil(T / (C - (2W+1))) (Sec. 2);
+                            > 0 is an explicit anchor period.                */
+  int32_t window_mode;   /* LVSA_WINDOW_*                                    */
+  int32_t rotate;        /* 1: anchors G^s of Eq. 3 (rotate with the step);
+                            0: Def. 2's fixed G = {t : t mod T_per = 0}.     */
+  int32_t tie_high;      /* Alg. 1 leaves equal room unresolved: 0 extends the
+                            low side (default), 1 the high side.            */
+} lvsa_params;
+
+/* Fills *p with C = 21, W = 6, tper = 0, EXPANDED, rotate = 1, tie_high = 0.
+ * C = 21 is the paper's Wan 2.1 budget ((81-1)/4 + 1 frames); the paper does
+ * not print W, and 6 is the smallest W that keeps |A(t)| within two frames of
+ * C and Alg. 1 within eight iterations on every Wan horizon. */
+void lvsa_params_default(lvsa_params* p);
+
+/* Frame-level sets for one denoising step (Def. 2, Eq. 3, Alg. 1).
+ *   T       frames, 1 <= T <= LVSA_MAX_FRAMES
+ *   step    denoising step s >= 0 (the same s for every layer and for the
+ *           conditional and unconditional passes)
+ * Outputs (host memory, caller-owned; any may be NULL to skip it):
+ *   tper_out      the anchor period T_per used
+ *   anchors       [T] ascending anchor frames; *n_anchors = |G^s| = ceil(T/T_per)
+ *   win_lo/win_hi [T] window bounds per query frame, so that
+ *                 A(t) = anchors  U  [win_lo[t], win_hi[t]]
+ * Errors: EINVAL for T, step or params out of range (including C <= 2W+1
+ * with tper == 0, and a null params pointer). */
+#define LVSA_MAX_FRAMES 4096
+lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
+                            int32_t* tper_out, int32_t* anchors,
+                            int32_t* n_anchors, int32_t* win_lo,
+                            int32_t* win_hi);
+
+/* ---------------------------------------------------------- block CSR ---- */
+
+/* Token i (0 <= i < N = T*P) lies in frame i / P and block i / B; there are
+ * nb = ceil(N / B) query blocks and nb key blocks, the last possibly ragged.
+ * Query block qb keeps key block kb iff some token of qb and some token of kb
+ * lie in frames t, tau with tau in A(t) (Eq. 2 applied to whole blocks: every
+ * attended token pair is covered; a block straddling a frame edge brings the
+ * rest of its tokens along).  Rows list kb in ascending order, without
+ * repeats, and always contain the diagonal block.  The mask does not depend
+ * on the head or the layer. */
+typedef struct lvsa_csr lvsa_csr; /* opaque, library-owned */
+
+/* Host builder (the paper builds this metadata on the CPU once per step).
+ *   T >= 1 frames (<= LVSA_MAX_FRAMES), P >= 1 tokens per frame,
+ *   1 <= B <= 2^20 tokens per block (the attention kernels take 64 or 128),
+ *   T*P + B < 2^31 and nb*nb < 2^31 (so nnz fits int32), step >= 0,
+ *   layer >= 0 (accepted, no effect).
+ * On LVSA_OK, *out owns host arrays row_ptr[nb+1] and col_idx[nnz] (int32);
+ * release it with lvsa_csr_free.  Errors: EINVAL (ranges, null pointers,
+ * params), ENOMEM.  *out is set to NULL on error. */
+lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
+                            int32_t layer, const lvsa_params* p,
+                            lvsa_csr** out);
+
+/* Read-only view of a handle's host arrays (pointers stay valid until
+ * lvsa_csr_free).  Any output pointer may be NULL. */
+lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
+                          int32_t* block, int32_t* n_blocks, int64_t* nnz,
+                          const int32_t** row_ptr, const int32_t** col_idx);
+
+/* Copies the host arrays to device memory owned by the handle (allocated on
+ * the first call, on the current device), asynchronously on `stream`; the
+ * host arrays must stay unmodified until the stream reaches the copy, which
+ * lvsa_csr_free respects by synchronizing the device before releasing.
+ * Errors: EINVAL (null), ENOMEM, EDEVICE. */
+lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream);
+
+/* Releases host and device memory of the handle.  NULL is accepted. */
+void lvsa_csr_free(lvsa_csr* csr);
+
+/* Device-resident block CSR: what the attention kernel reads.  Fill it from
+ * an uploaded handle with lvsa_csr_device_view, or point it at buffers
+ * written by lvsa_build_mask_device. */
+typedef struct lvsa_block_mask {
+  int32_t n_tokens;       /* N                                             */
+  int32_t block;          /* B, tokens per query block and per key block  */
+  int32_t n_blocks;       /* nb = ceil(N / B)                              */
+  const int32_t* row_ptr; /* device, [nb + 1], row_ptr[0] = 0, ascending   */
+  const int32_t* col_idx; /* device, [row_ptr[nb]], each row ascending     */
+} lvsa_block_mask;
+
+/* Errors: EINVAL if the handle was never uploaded. */
+lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
+
+/* Device builder: the same mask computed by one kernel on `stream`, written
+ * to caller-owned device buffers (no host round trip, no allocation).
+ *   d_row_ptr    device int32[nb + 1]
+ *   d_col_idx    device int32[col_capacity]; col_capacity must be at least
+ *                nb * nb (the mask's worst case), so every write is in bounds
+ * Arguments as for lvsa_build_mask; T <= LVSA_MAX_FRAMES.
+ * Errors: EINVAL (ranges, nulls, capacity), EDEVICE (launch). */
+lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
+                                   int32_t step, int32_t layer,
+                                   const lvsa_params* p, int32_t* d_row_ptr,
+                                   int32_t* d_col_idx, int64_t col_capacity,
+                                   void* stream);
+
+/* --------------------------------------------------------- attention ---- */
+
+/* A bf16 tensor [heads, n_tokens, head_dim] in device memory.  Element
+ * (h, i, c) is at data + h*stride_head + i*stride_token + c (elements; the
+ * head_dim stride is 1).  data must be 16-byte aligned and stride_token and
+ * stride_head multiples of 8. */
+typedef struct lvsa_tensor {
+  void* data;
+  int32_t heads;
+  int32_t n_tokens;
+  int32_t head_dim;
+  int64_t stride_head;
+  int64_t stride_token;
+} lvsa_tensor;
+
+/* Block-sparse attention forward (Eq. 2 over the kept blocks of `mask`):
+ *   out[h, i] = sum_j softmax_j(q[h,i] . k[h,j] / sqrt(d)) v[h,j]
+ * with j over the real tokens (j < N) of the key blocks kept for the query
+ * block of i.  bf16 inputs, fp32 products and softmax, bf16 output (round to
+ * nearest even).  q, k, v, out share heads, n_tokens = mask->n_tokens and
+ * head_dim = 128; mask->block is 64 or 128.  Rows i >= N of `out` are never
+ * written.  out must not overlap q, k or v.  The result is deterministic
+ * (fixed key order per row).
+ * Errors: EINVAL (nulls, shape mismatch), EUNSUPPORTED (head_dim, block,
+ * alignment), EDEVICE (launch). */
+lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
+                           const lvsa_tensor* v, const lvsa_block_mask* mask,
+                           lvsa_tensor* out, void* stream);
+
+/* Dense attention forward (Eq. 1 over all N keys), the same kernel design
+ * visiting every key block; `block` (64 or 128) is its tile size.
+ * Errors as for lvsa_attention. */
+lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
+                                 const lvsa_tensor* v, int32_t block,
+                                 lvsa_tensor* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LVSA_H */

@@ -1,0 +1,301 @@
+// api.cpp -- the C ABI declared in include/lvsa.h: argument checks, handle
+// management and dispatch to the builders and kernels.
+#include <climits>
+#include <new>
+
+#include "internal.h"
+
+namespace lvsa {
+
+lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
+                           FrameCfg* out) {
+  if (!p || !out) return LVSA_EINVAL;
+  if (T < 1 || T > LVSA_MAX_FRAMES || step < 0) return LVSA_EINVAL;
+  if (p->window < 0 || p->window > LVSA_MAX_FRAMES) return LVSA_EINVAL;
+  if (p->window_mode < LVSA_WINDOW_BASIC || p->window_mode > LVSA_WINDOW_EXPANDED)
+    return LVSA_EINVAL;
+  if ((p->rotate != 0 && p->rotate != 1) || (p->tie_high != 0 && p->tie_high != 1))
+    return LVSA_EINVAL;
+  if (p->tper < 0) return LVSA_EINVAL;
+  int32_t tper = p->tper;
+  if (tper == 0) {
+    // Sec. 2, budget paragraph: T_per = ceil(T / (C - (2W+1))), for C > 2W+1.
+    const int32_t spare = p->budget_frames - (2 * p->window + 1);
+    if (p->budget_frames <= 0 || spare <= 0) return LVSA_EINVAL;
+    tper = ceil_div(T, spare);
+  }
+  FrameCfg c;
+  c.T = T;
+  c.W = p->window;
+  c.tper = tper;
+  c.k = ceil_div(T, tper);
+  c.s0 = p->rotate ? step % tper : 0;
+  c.mode = p->window_mode;
+  c.rotate = p->rotate;
+  c.tie_high = p->tie_high;
+  *out = c;
+  return LVSA_OK;
+}
+
+lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B) {
+  if (T < 1 || P < 1 || B < 1 || B > (1 << 20)) return LVSA_EINVAL;
+  const int64_t N = (int64_t)T * P;
+  if (N + B > INT32_MAX) return LVSA_EINVAL;
+  const int64_t nb = (N + B - 1) / B;
+  if (nb * nb > INT32_MAX) return LVSA_EINVAL;  // nnz must fit row_ptr
+  return LVSA_OK;
+}
+
+}  // namespace lvsa
+
+struct lvsa_csr {
+  int32_t n_tokens = 0;
+  int32_t block = 0;
+  int32_t n_blocks = 0;
+  std::vector<int32_t> row_ptr;
+  std::vector<int32_t> col_idx;
+  int32_t* d_row_ptr = nullptr;
+  int32_t* d_col_idx = nullptr;
+  int64_t d_col_cap = 0;
+};
+
+using namespace lvsa;
+
+extern "C" {
+
+const char* lvsa_status_str(lvsa_status s) {
+  switch (s) {
+    case LVSA_OK: return "ok";
+    case LVSA_EINVAL: return "invalid argument";
+    case LVSA_ENOMEM: return "out of memory";
+    case LVSA_EDEVICE: return "device error";
+    case LVSA_EUNSUPPORTED: return "unsupported shape or layout";
+    default: return "unknown status";
+  }
+}
+
+int32_t lvsa_version(void) { return 100; }
+
+void lvsa_params_default(lvsa_params* p) {
+  if (!p) return;
+  p->budget_frames = 21;
+  p->window = 6;
+  p->tper = 0;
+  p->window_mode = LVSA_WINDOW_EXPANDED;
+  p->rotate = 1;
+  p->tie_high = 0;
+}
+
+lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
+                            int32_t* tper_out, int32_t* anchors,
+                            int32_t* n_anchors, int32_t* win_lo,
+                            int32_t* win_hi) {
+  FrameCfg c;
+  const lvsa_status st = resolve_frames(T, step, p, &c);
+  if (st != LVSA_OK) return st;
+  if (tper_out) *tper_out = c.tper;
+  int32_t n = 0;
+  for (int32_t t = 0; t < T; ++t)
+    if (is_anchor(c, t)) {
+      if (anchors) anchors[n] = t;
+      ++n;
+    }
+  if (n_anchors) *n_anchors = n;
+  for (int32_t t = 0; t < T; ++t) {
+    int32_t lo, hi;
+    frame_window(c, t, &lo, &hi);
+    if (win_lo) win_lo[t] = lo;
+    if (win_hi) win_hi[t] = hi;
+  }
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
+                            int32_t layer, const lvsa_params* p,
+                            lvsa_csr** out) {
+  if (!out) return LVSA_EINVAL;
+  *out = nullptr;
+  if (layer < 0) return LVSA_EINVAL;
+  lvsa_status st = check_mask_shape(T, P, B);
+  if (st != LVSA_OK) return st;
+  FrameCfg c;
+  st = resolve_frames(T, step, p, &c);
+  if (st != LVSA_OK) return st;
+  lvsa_csr* h = new (std::nothrow) lvsa_csr();
+  if (!h) return LVSA_ENOMEM;
+  try {
+    build_csr_host(c, P, B, &h->row_ptr, &h->col_idx);
+  } catch (const std::bad_alloc&) {
+    delete h;
+    return LVSA_ENOMEM;
+  }
+  h->n_tokens = T * P;
+  h->block = B;
+  h->n_blocks = (int32_t)h->row_ptr.size() - 1;
+  *out = h;
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
+                          int32_t* block, int32_t* n_blocks, int64_t* nnz,
+                          const int32_t** row_ptr, const int32_t** col_idx) {
+  if (!csr) return LVSA_EINVAL;
+  if (n_tokens) *n_tokens = csr->n_tokens;
+  if (block) *block = csr->block;
+  if (n_blocks) *n_blocks = csr->n_blocks;
+  if (nnz) *nnz = (int64_t)csr->col_idx.size();
+  if (row_ptr) *row_ptr = csr->row_ptr.data();
+  if (col_idx) *col_idx = csr->col_idx.data();
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
+  if (!csr) return LVSA_EINVAL;
+  const int64_t nnz = (int64_t)csr->col_idx.size();
+  if (!csr->d_row_ptr) {
+    if (hipMalloc(&csr->d_row_ptr, sizeof(int32_t) * csr->row_ptr.size()) !=
+        hipSuccess) {
+      csr->d_row_ptr = nullptr;
+      return LVSA_ENOMEM;
+    }
+  }
+  if (!csr->d_col_idx || csr->d_col_cap < nnz) {
+    if (csr->d_col_idx) (void)hipFree(csr->d_col_idx);
+    csr->d_col_idx = nullptr;
+    csr->d_col_cap = 0;
+    const int64_t cap = nnz > 0 ? nnz : 1;
+    if (hipMalloc(&csr->d_col_idx, sizeof(int32_t) * cap) != hipSuccess) {
+      csr->d_col_idx = nullptr;
+      return LVSA_ENOMEM;
+    }
+    csr->d_col_cap = cap;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(csr->d_row_ptr, csr->row_ptr.data(),
+                     sizeof(int32_t) * csr->row_ptr.size(),
+                     hipMemcpyHostToDevice, s) != hipSuccess)
+    return LVSA_EDEVICE;
+  if (nnz > 0 &&
+      hipMemcpyAsync(csr->d_col_idx, csr->col_idx.data(), sizeof(int32_t) * nnz,
+                     hipMemcpyHostToDevice, s) != hipSuccess)
+    return LVSA_EDEVICE;
+  return LVSA_OK;
+}
+
+void lvsa_csr_free(lvsa_csr* csr) {
+  if (!csr) return;
+  if (csr->d_row_ptr || csr->d_col_idx) {
+    (void)hipDeviceSynchronize();
+    if (csr->d_row_ptr) (void)hipFree(csr->d_row_ptr);
+    if (csr->d_col_idx) (void)hipFree(csr->d_col_idx);
+  }
+  delete csr;
+}
+
+lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out) {
+  if (!csr || !out || !csr->d_row_ptr || !csr->d_col_idx) return LVSA_EINVAL;
+  out->n_tokens = csr->n_tokens;
+  out->block = csr->block;
+  out->n_blocks = csr->n_blocks;
+  out->row_ptr = csr->d_row_ptr;
+  out->col_idx = csr->d_col_idx;
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
+                                   int32_t step, int32_t layer,
+                                   const lvsa_params* p, int32_t* d_row_ptr,
+                                   int32_t* d_col_idx, int64_t col_capacity,
+                                   void* stream) {
+  if (layer < 0 || !d_row_ptr || !d_col_idx) return LVSA_EINVAL;
+  lvsa_status st = check_mask_shape(T, P, B);
+  if (st != LVSA_OK) return st;
+  FrameCfg c;
+  st = resolve_frames(T, step, p, &c);
+  if (st != LVSA_OK) return st;
+  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  if (col_capacity < nb * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx,
+                               (hipStream_t)stream) != hipSuccess)
+    return LVSA_EDEVICE;
+  return LVSA_OK;
+}
+
+namespace {
+
+lvsa_status check_tensor(const lvsa_tensor* t, int32_t heads, int32_t n) {
+  if (!t || !t->data) return LVSA_EINVAL;
+  if (t->heads != heads || t->n_tokens != n) return LVSA_EINVAL;
+  if (t->head_dim != 128) return LVSA_EUNSUPPORTED;
+  if (((uintptr_t)t->data) % 16 != 0) return LVSA_EUNSUPPORTED;
+  if (t->stride_token < 1 || t->stride_token % 8 != 0) return LVSA_EUNSUPPORTED;
+  if (t->stride_head < 0 || t->stride_head % 8 != 0) return LVSA_EUNSUPPORTED;
+  return LVSA_OK;
+}
+
+lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
+                          const lvsa_tensor* v, int32_t n_tokens,
+                          int32_t block, int32_t n_blocks,
+                          const int32_t* row_ptr, const int32_t* col_idx,
+                          bool sparse, lvsa_tensor* out, void* stream) {
+  if (!q || !k || !v || !out) return LVSA_EINVAL;
+  if (block != 64 && block != 128) return LVSA_EUNSUPPORTED;
+  const int32_t H = q->heads;
+  if (H < 1 || n_tokens < 1) return LVSA_EINVAL;
+  if (n_blocks != (int32_t)(((int64_t)n_tokens + block - 1) / block))
+    return LVSA_EINVAL;
+  // Work-items per launch must stay below 2^32.
+  if ((int64_t)n_blocks * H * block * 2 >= ((int64_t)1 << 32)) return LVSA_EUNSUPPORTED;
+  lvsa_status st;
+  if ((st = check_tensor(q, H, n_tokens)) != LVSA_OK) return st;
+  if ((st = check_tensor(k, H, n_tokens)) != LVSA_OK) return st;
+  if ((st = check_tensor(v, H, n_tokens)) != LVSA_OK) return st;
+  if ((st = check_tensor(out, H, n_tokens)) != LVSA_OK) return st;
+  if (out->data == q->data || out->data == k->data || out->data == v->data)
+    return LVSA_EINVAL;
+  AttnArgs a;
+  a.q = q->data;
+  a.k = k->data;
+  a.v = v->data;
+  a.o = out->data;
+  a.q_sh = q->stride_head;
+  a.q_st = q->stride_token;
+  a.k_sh = k->stride_head;
+  a.k_st = k->stride_token;
+  a.v_sh = v->stride_head;
+  a.v_st = v->stride_token;
+  a.o_sh = out->stride_head;
+  a.o_st = out->stride_token;
+  a.heads = H;
+  a.n_tokens = n_tokens;
+  a.n_blocks = n_blocks;
+  a.row_ptr = row_ptr;
+  a.col_idx = col_idx;
+  if (launch_attention(a, block, sparse, (hipStream_t)stream) != hipSuccess)
+    return LVSA_EDEVICE;
+  return LVSA_OK;
+}
+
+}  // namespace
+
+lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
+                           const lvsa_tensor* v, const lvsa_block_mask* mask,
+                           lvsa_tensor* out, void* stream) {
+  if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
+  return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
+                       mask->row_ptr, mask->col_idx, true, out, stream);
+}
+
+lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
+                                 const lvsa_tensor* v, int32_t block,
+                                 lvsa_tensor* out, void* stream) {
+  if (!q) return LVSA_EINVAL;
+  if (block != 64 && block != 128) return LVSA_EUNSUPPORTED;
+  const int32_t n = q->n_tokens;
+  if (n < 1) return LVSA_EINVAL;
+  const int32_t nb = (int32_t)(((int64_t)n + block - 1) / block);
+  return run_attention(q, k, v, n, block, nb, nullptr, nullptr, false, out,
+                       stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// frames.h -- LVSA frame-level rules shared by the host and device mask
+// builders (LVSA paper, Sec. 2: Def. 2, Eq. 3, the adaptive window and
+// Alg. 1).  Everything here is integer arithmetic on frame indices, written
+// once as __host__ __device__ inline functions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lvsa.h"
+
+namespace lvsa {
+
+// Resolved per-step frame configuration.
+struct FrameCfg {
+  int32_t T;         // frames
+  int32_t W;         // window half-width
+  int32_t tper;      // anchor period T_per
+  int32_t k;         // |G^s| = ceil(T / T_per)
+  int32_t s0;        // s mod T_per (0 for fixed anchors)
+  int32_t mode;      // LVSA_WINDOW_*
+  int32_t rotate;    // Eq. 3 (1) or Def. 2's fixed set (0)
+  int32_t tie_high;  // Alg. 1 equal-room rule
+};
+
+__host__ __device__ inline int32_t ceil_div(int32_t a, int32_t b) {
+  return (a + b - 1) / b;
+}
+__host__ __device__ inline int32_t imin(int32_t a, int32_t b) { return a < b ? a : b; }
+__host__ __device__ inline int32_t imax(int32_t a, int32_t b) { return a > b ? a : b; }
+
+// Membership of frame f in the anchor set.
+//   rotate = 0: Def. 2, f mod T_per == 0.
+//   rotate = 1: Eq. 3, f = (s0 + i*T_per) mod T for some 0 <= i < k.  The
+//   unreduced value s0 + i*T_per is below k*T_per <= T + T_per - 1 < 2T, so
+//   it equals either f or f + T.
+__host__ __device__ inline bool is_anchor(const FrameCfg& c, int32_t f) {
+  if (!c.rotate) return f % c.tper == 0;
+  if (f >= c.s0 && (f - c.s0) % c.tper == 0 && (f - c.s0) / c.tper < c.k)
+    return true;
+  const int32_t u = f + c.T - c.s0;
+  return u % c.tper == 0 && u / c.tper < c.k;
+}
+
+// Window [lo, hi] of query frame t under the configured rule.
+//   BASIC    Def. 2
+//   ADAPTIVE shifted to keep 2W+1 frames (Sec. 2, "Overlapping frames")
+//   EXPANDED Alg. 1: grow the adaptive window on the side with more room
+//            until min(2W+1, T-|G|) of its frames are not anchors.
+// Returns the number of Alg. 1 growth steps (0 for the other rules).
+__host__ __device__ inline int32_t frame_window(const FrameCfg& c, int32_t t,
+                                                int32_t* lo_out,
+                                                int32_t* hi_out) {
+  const int32_t T = c.T, W = c.W;
+  int32_t lo, hi;
+  if (c.mode == LVSA_WINDOW_BASIC) {
+    lo = imax(0, t - W);
+    hi = imin(T - 1, t + W);
+    *lo_out = lo;
+    *hi_out = hi;
+    return 0;
+  }
+  lo = imax(0, imin(t - W, T - 1 - 2 * W));
+  hi = imin(T - 1, imax(t + W, 2 * W));
+  int32_t steps = 0;
+  if (c.mode == LVSA_WINDOW_EXPANDED) {
+    const int32_t target = imin(2 * W + 1, T - c.k);
+    int32_t nonglobal = 0;
+    for (int32_t f = lo; f <= hi; ++f) nonglobal += is_anchor(c, f) ? 0 : 1;
+    while (nonglobal < target && (lo > 0 || hi < T - 1)) {
+      const int32_t room_lo = lo, room_hi = T - 1 - hi;
+      int32_t f;
+      if (room_lo > room_hi || (room_lo == room_hi && !c.tie_high))
+        f = --lo;
+      else
+        f = ++hi;
+      nonglobal += is_anchor(c, f) ? 0 : 1;
+      ++steps;
+    }
+  }
+  *lo_out = lo;
+  *hi_out = hi;
+  return steps;
+}
+
+// First and last frame touched by block b (tokens b*B .. min((b+1)*B, N)-1).
+__host__ __device__ inline void block_frame_range(int32_t b, int32_t P,
+                                                  int32_t B, int32_t N,
+                                                  int32_t* first,
+                                                  int32_t* last) {
+  const int64_t t0 = (int64_t)b * B;
+  const int64_t end = t0 + B < (int64_t)N ? t0 + B : (int64_t)N;
+  *first = (int32_t)(t0 / P);
+  *last = (int32_t)((end - 1) / P);
+}
+
+}  // namespace lvsa

@@ -1,0 +1,48 @@
+// internal.h -- declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "frames.h"
+#include "lvsa.h"
+
+namespace lvsa {
+
+// Checks the mask arguments and resolves T_per, |G^s| and s mod T_per.
+lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
+                           FrameCfg* out);
+
+// Checks (T, P, B) of a block mask: T*P + B must fit in int32.
+lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B);
+
+// Host CSR construction (mask_host.cpp).
+void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
+                    std::vector<int32_t>* row_ptr,
+                    std::vector<int32_t>* col_idx);
+
+// Device CSR construction (mask_device.hip).
+hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
+                                    int32_t* d_row_ptr, int32_t* d_col_idx,
+                                    hipStream_t stream);
+
+// Attention launch (attention.hip).  Pointers are bf16 tensors; strides in
+// elements.  row_ptr/col_idx are null for the dense pass.
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  int64_t q_sh, q_st, k_sh, k_st, v_sh, v_st, o_sh, o_st;
+  int32_t heads;
+  int32_t n_tokens;
+  int32_t n_blocks;
+  const int32_t* row_ptr;
+  const int32_t* col_idx;
+};
+hipError_t launch_attention(const AttnArgs& a, int32_t block, bool sparse,
+                            hipStream_t stream);
+
+}  // namespace lvsa

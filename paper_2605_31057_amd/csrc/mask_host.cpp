@@ -1,0 +1,70 @@
+// mask_host.cpp -- host LVSA mask builder: frame sets -> block CSR.
+//
+// The paper builds the index metadata on the CPU once per denoising step
+// (Sec. 2, cost remark after Alg. 1 and the end of "Rotating periodic global
+// frames").  Query block qb keeps key block kb iff some frame t touched by qb
+// and some frame tau touched by kb have tau in A(t), where
+// A(t) = G^s U [lo(t), hi(t)].
+//
+// For each query block the attended frames are gathered into a T-entry
+// flag array, then each attended frame contributes its block range
+// [tau*P/B, ((tau+1)*P-1)/B]; ranges come in ascending order and overlap only
+// at a shared straddling block, so a running "last emitted" index keeps the
+// row ascending and free of repeats.  Consecutive query blocks that touch
+// the same frames have identical rows, which are copied.
+#include <algorithm>
+#include <cstring>
+
+#include "internal.h"
+
+namespace lvsa {
+
+void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
+                    std::vector<int32_t>* row_ptr,
+                    std::vector<int32_t>* col_idx) {
+  const int32_t T = c.T;
+  const int32_t N = T * P;
+  const int32_t nb = ceil_div(N, B);
+  std::vector<int32_t> lo(T), hi(T);
+  std::vector<uint8_t> anchor(T);
+  for (int32_t t = 0; t < T; ++t) {
+    anchor[t] = is_anchor(c, t) ? 1 : 0;
+    frame_window(c, t, &lo[t], &hi[t]);
+  }
+  row_ptr->assign(nb + 1, 0);
+  col_idx->clear();
+  col_idx->reserve((size_t)nb * 64);
+  std::vector<uint8_t> attended(T);
+  int32_t prev_first = -1, prev_last = -1;
+  int64_t prev_begin = 0, prev_len = 0;
+  for (int32_t qb = 0; qb < nb; ++qb) {
+    int32_t f0, f1;
+    block_frame_range(qb, P, B, N, &f0, &f1);
+    const int64_t begin = (int64_t)col_idx->size();
+    if (f0 == prev_first && f1 == prev_last) {
+      col_idx->resize(begin + prev_len);
+      std::memcpy(col_idx->data() + begin, col_idx->data() + prev_begin,
+                  prev_len * sizeof(int32_t));
+    } else {
+      std::memcpy(attended.data(), anchor.data(), T);
+      for (int32_t t = f0; t <= f1; ++t)
+        std::fill(attended.begin() + lo[t], attended.begin() + hi[t] + 1, 1);
+      int32_t last = -1;
+      for (int32_t tau = 0; tau < T; ++tau) {
+        if (!attended[tau]) continue;
+        const int32_t b0 = (int32_t)((int64_t)tau * P / B);
+        const int32_t b1 = (int32_t)(((int64_t)tau * P + P - 1) / B);
+        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b)
+          col_idx->push_back(b);
+        last = std::max(last, b1);
+      }
+      prev_first = f0;
+      prev_last = f1;
+    }
+    prev_begin = begin;
+    prev_len = (int64_t)col_idx->size() - begin;
+    (*row_ptr)[qb + 1] = (int32_t)col_idx->size();
+  }
+}
+
+}  // namespace lvsa

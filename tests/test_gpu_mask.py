@@ -1,0 +1,89 @@
+"""GPU parity: the device mask builder's CSR equals the oracle's bit for bit,
+and attention over it equals attention over the host-built CSR bit for bit."""
+import random
+import sys
+
+import pytest
+import torch
+
+import paper_2605_31057_amd as L
+from paper_2605_31057_amd.inputs import WORKLOADS, make_qkv
+from oracle import mask as M
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    L.lib()
+
+
+def _device_csr(T, P, B, step, p, layer=0):
+    nb = -(-(T * P) // B)
+    rp = torch.full((nb + 1,), -1, dtype=torch.int32, device="cuda")
+    ci = torch.full((nb * nb,), -1, dtype=torch.int32, device="cuda")
+    L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer)
+    torch.cuda.synchronize()
+    rp = rp.cpu()
+    nnz = int(rp[-1])
+    return rp.tolist(), ci[:nnz].cpu().tolist(), ci
+
+
+def _kw(p):
+    return dict(C=p.budget_frames, W=p.window, tper=p.tper, mode=p.window_mode,
+                rotate=bool(p.rotate), tie_high=bool(p.tie_high))
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_device_builder_matches_oracle_workloads(name):
+    w = WORKLOADS[name]
+    p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    steps = list(w.steps) if len(w.steps) > 1 else [0, 1, 10, 17]
+    print(f"[mask] {name} steps {steps[0]}..{steps[-1]}", flush=True)
+    for s in steps:
+        for layer in w.layers:
+            rp, ci, raw = _device_csr(w.frames, w.tokens_per_frame, w.block, s, p, layer)
+            want_rp, want_ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, s,
+                                            layer=layer, **_kw(p))
+            assert rp == want_rp, (name, s, layer)
+            assert ci == want_ci, (name, s, layer)
+            # nothing written past nnz
+            assert bool((raw[len(ci):] == -1).all())
+
+
+@pytest.mark.parametrize("mode", [L.WINDOW_BASIC, L.WINDOW_ADAPTIVE, L.WINDOW_EXPANDED])
+def test_device_builder_matches_oracle_random(mode):
+    rng = random.Random(77 + mode)
+    print(f"[mask] random mode {mode}", flush=True)
+    for _ in range(40):
+        T = rng.randint(1, 60)
+        p = L.Params(window=rng.randint(0, 6), tper=rng.randint(1, T), window_mode=mode,
+                     rotate=rng.randint(0, 1), tie_high=rng.randint(0, 1))
+        P = rng.randint(1, 300)
+        B = rng.choice([1, 3, 16, 64, 128])
+        if -(-(T * P) // B) > 1500:
+            B = 64
+        s = rng.randint(0, 40)
+        rp, ci, _ = _device_csr(T, P, B, s, p)
+        want_rp, want_ci = M.build_mask(T, P, B, s, **_kw(p))
+        assert rp == want_rp and ci == want_ci, (T, P, B, s)
+
+
+def test_device_mask_attention_equals_host_mask_attention():
+    T, P, B, H = 9, 333, 128, 2
+    print("[mask] device-CSR attention vs host-CSR attention", flush=True)
+    q, k, v = (x.cuda() for x in make_qkv(H, T * P, seed=3))
+    p = L.Params(budget_frames=7, window=1)
+    for s in (0, 1, 2):
+        csr = L.build_mask(T, P, B, s, p)
+        csr.upload()
+        a = L.attention(q, k, v, csr.device_mask())
+        nb = -(-(T * P) // B)
+        rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+        ci = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+        m = L.build_mask_device(T, P, B, s, rp, ci, params=p)
+        b = L.attention(q, k, v, m)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
