@@ -133,6 +133,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--pmc", action="store_true",
+                    help="counter-collection run: a few untimed sparse, dense and "
+                         "mask launches plus a 1 GiB copy (the byte-counter "
+                         "calibration), for rocprofv3 --pmc")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -168,6 +172,22 @@ def main():
         csr.free()
     dense_flops = kept_flops(np.arange(nb + 1) * nb, np.tile(np.arange(nb), nb),
                              w.n_tokens, w.block, w.heads)
+
+    if args.pmc:
+        m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, 10, rp, ci,
+                                params=params, stream=stream)
+        for _ in range(3):
+            L.attention(q, k, v, m, out=out, stream=stream)
+        if not args.no_dense:
+            L.dense_attention(q, k, v, block=w.block, out=out, stream=stream)
+        src = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print("[bench] pmc launches done (copy calibration: 1 GiB read, 1 GiB "
+              "written per copy)", file=sys.stderr, flush=True)
+        return
 
     def step(i):
         s = w.steps[i % n_sweep]
