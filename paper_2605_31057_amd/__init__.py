@@ -150,8 +150,8 @@ class Csr:
         self.free()
 
     def free(self):
-        if getattr(self, "_h", None) and self._h.value:
-            lib().lvsa_csr_free(self._h)
+        if getattr(self, "_h", None) and self._h.value and _LIB is not None:
+            _LIB.lvsa_csr_free(self._h)
             self._h = _p()
 
     def info(self):

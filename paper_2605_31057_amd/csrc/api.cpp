@@ -251,6 +251,11 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   if ((st = check_tensor(k, H, n_tokens)) != LVSA_OK) return st;
   if ((st = check_tensor(v, H, n_tokens)) != LVSA_OK) return st;
   if ((st = check_tensor(out, H, n_tokens)) != LVSA_OK) return st;
+  // K and V rows are addressed with 32-bit byte offsets within a head.
+  const int64_t rows = (int64_t)n_blocks * block;
+  if (rows * k->stride_token * 2 >= ((int64_t)1 << 32) ||
+      rows * v->stride_token * 2 >= ((int64_t)1 << 32))
+    return LVSA_EUNSUPPORTED;
   if (out->data == q->data || out->data == k->data || out->data == v->data)
     return LVSA_EINVAL;
   AttnArgs a;
