@@ -18,9 +18,8 @@
 //   register staging), double-buffered: the next key block is in flight while
 //   the current one is consumed.  The buffer resource's size bound turns rows
 //   at or past N (the ragged last block) into zeros.  16-byte chunks of each
-//   LDS row are XOR-swizzled so both the K reads (ds_read_b128, 32 rows of one
-//   chunk) and the V reads (ds_read_b64_tr_b16, 8 rows x 4 chunks) are free of
-//   bank conflicts.
+//   LDS row are XOR-swizzled so both the K reads (ds_read_b128) and the V
+//   reads (ds_read_b64_tr_b16) are free of bank conflicts.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS), B = Q rows (registers, loaded once)
@@ -66,8 +65,13 @@ __device__ inline int xcd_remap(int bid, int total) {
          idx;
 }
 
-// Swizzle of the 16-byte chunk index within an LDS row.
-__device__ inline int swz(int row) { return ((row & 7) << 1) | ((row >> 3) & 1); }
+// Swizzle of the 16-byte chunk index within a 256-byte LDS row.  LDS has 64
+// banks of 4 bytes.  ds_read_b128 is served 16 lanes at a time: here 16
+// consecutive rows at one logical chunk, which the swizzle spreads over all
+// 16 chunk positions.  ds_read_b64_tr_b16 is served 32 lanes at a time: here
+// 4 consecutive rows x 4 adjacent logical chunks, which the swizzle places in
+// 4 disjoint groups of 4 chunk positions (bits 2-3 of the XOR follow row%4).
+__device__ inline int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base,
                                                    uint32_t bytes) {
@@ -221,7 +225,8 @@ __device__ inline void consume(const __bf16* lds_k, const __bf16* lds_v,
   const int vrow0 = TL::KH * kh + 4 * (g / 2) + sl / 4;
   const int cb = 2 * (g % 2) + (sl % 4) / 2;
   const int half = (sl % 2) * 8;
-  const int f0 = swz(vrow0);  // even: vrow0 % 16 < 8 here
+  const int f0 = swz(vrow0);
+  const int f1 = swz(vrow0 + 8);
 #pragma unroll
   for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
@@ -235,7 +240,7 @@ __device__ inline void consume(const __bf16* lds_k, const __bf16* lds_v,
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (lds_i16x4*)(r0 + pc0 * 16));
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(r1 + (pc0 ^ 1) * 16));
+            (lds_i16x4*)(r1 + ((4 * dt + cb) ^ f1) * 16));
         const bf16x8 a = __builtin_bit_cast(
             bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kt][c],
