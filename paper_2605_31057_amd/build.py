@@ -24,6 +24,9 @@ CFLAGS = [
     "-Wall", "-Wno-unused-result",
     # Keep the compiler from forming packed fp32 VALU instructions.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # Keep MFMA results in VGPRs where possible: the attention scores are
+    # consumed by VALU code, and AGPR homes for them cost a copy per element.
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 

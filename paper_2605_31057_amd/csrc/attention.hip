@@ -5,29 +5,28 @@
 // (all keys) with the same kernel visiting every key block.
 //
 // Work decomposition
-//   One workgroup per (head, query block of BLOCK rows), 2*BLOCK/32 waves
-//   (two per SIMD at BLOCK = 128).  Wave w owns query rows 32*(w % R) ..+31
-//   (R = BLOCK/32 row groups) and key half w / R of every key block: the two
-//   waves of a row group run independent online softmaxes over disjoint keys
-//   and are merged once at the end.  Two waves per SIMD let one wave's MFMAs
-//   overlap the other's softmax arithmetic.
+//   One workgroup per (head, query block of BLOCK rows); 2*BLOCK/64 waves, one
+//   per SIMD at BLOCK = 128.  Wave w owns 64 query rows (row group w % RG, as
+//   two 32-row MFMA tiles) and one half of the keys of every key block
+//   (w / RG).  The two waves of a row group keep independent online softmax
+//   states over disjoint keys and are merged once at the end.  Holding 64 rows
+//   per wave lets every K and V fragment read from LDS feed two MFMAs.
 //
-// Data movement
-//   Key blocks are visited in CSR order.  K and V tiles (BLOCK x 128 bf16,
-//   row-major) go HBM/L2 -> LDS by buffer loads that write LDS directly (no
-//   register staging), double-buffered: the next key block is in flight while
-//   the current one is consumed.  The buffer resource's size bound turns rows
-//   at or past N (the ragged last block) into zeros.  16-byte chunks of each
-//   LDS row are XOR-swizzled so both the K reads (ds_read_b128) and the V
-//   reads (ds_read_b64_tr_b16) are free of bank conflicts.
+// Pipeline (per wave, one key block per step)
+//   LDS holds two K stages and two V stages (slab layout, see below).  K runs one block ahead of V:
+//   during step j the wave computes S(j+1) = K(j+1) Q^T while it exponentiates
+//   S(j) and accumulates P(j) V(j), so MFMA and VALU work of one wave overlap;
+//   meanwhile K(j+2) and V(j+1) stream from HBM/L2 into the free stages with
+//   buffer loads that write LDS directly.  One barrier per step hands the
+//   stages over.  The buffer resource's size bound turns rows at or past N
+//   (ragged last block) into zeros.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
-//     S^T = K Q^T     A = K rows (LDS), B = Q rows (registers, loaded once)
-//     O^T += V^T P^T  A = V^T via the transposing LDS read, B = P from S^T's
-//                     registers
+//     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
+//     O^T += V^T P^T  A = V^T (LDS, ds_read_b64_tr_b16), B = P (registers)
 //   The transposed products put one query row per lane (lanes l and l^32
-//   share row l%32), so softmax row statistics are in-lane reductions plus
-//   one permlane32 exchange, and P never leaves registers.
+//   share row l%32), so row statistics are in-lane reductions plus one
+//   permlane32 exchange, and P never leaves registers.
 //   MFMA 32x32 lane layout (lane l, half h = l/32, i = l%32): A row i and B
 //   column i carry k-slots 8h..8h+7; C register r holds row 8*(r/4)+4h+(r%4),
 //   column i.  k-slot order only has to agree between A and B, so the key
@@ -51,11 +50,10 @@ constexpr int D = 128;             // head_dim
 constexpr int ROW_BYTES = D * 2;   // one K/V row in LDS
 constexpr float RESCALE_SLACK = 8.f;
 
-
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-__device__ inline int xcd_remap(int bid, int total) {
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
   // contiguous range of logical tiles so that neighbouring query blocks of a
   // head, whose key lists overlap, share that XCD's L2.
@@ -65,188 +63,369 @@ __device__ inline int xcd_remap(int bid, int total) {
          idx;
 }
 
-// Swizzle of the 16-byte chunk index within a 256-byte LDS row.  LDS has 64
-// banks of 4 bytes.  ds_read_b128 is served 16 lanes at a time: here 16
-// consecutive rows at one logical chunk, which the swizzle spreads over all
-// 16 chunk positions.  ds_read_b64_tr_b16 is served 32 lanes at a time: here
-// 4 consecutive rows x 4 adjacent logical chunks, which the swizzle places in
-// 4 disjoint groups of 4 chunk positions (bits 2-3 of the XOR follow row%4).
-__device__ inline int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
-
-__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base,
-                                                   uint32_t bytes) {
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base,
+                                                            uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
                                            bytes, 0x00020000);
 }
 
-__device__ inline float pair_max(float x) {
+__device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
                                             __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ inline float pair_sum(float x) {
+__device__ __forceinline__ float pair_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
                                             __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// LDS tile layout ("slabs").  A BLOCK x 128 tile is stored as 4 slabs of 32
+// columns; a slab row is 64 bytes (4 chunks of 16 bytes) and rows follow each
+// other, so tile byte (slab, row, chunk) = slab*BLOCK*64 + row*64 + chunk*16.
+// The chunk is XORed with x(row) = (row/4) % 4.  With 64 banks of 4 bytes:
+//   - ds_read_b128 (served 16 lanes at a time) reads 16 consecutive rows at
+//     one logical chunk: 4 rows share a bank window and the XOR separates them;
+//   - ds_read_b64_tr_b16 (served 32 lanes at a time) reads 4 consecutive rows
+//     x 4 chunks, i.e. 256 contiguous bytes.
+// Both are free of bank conflicts, and every fragment address an unrolled loop
+// needs is one of two per-lane bases plus an immediate offset.
+constexpr int SLAB_ROW = 64;
+__device__ __forceinline__ int xsw(int row) { return (row >> 2) & 3; }
+
+#ifndef LVSA_QT
+#define LVSA_QT 1
+#endif
+constexpr int QT = LVSA_QT;   // 32-row query tiles per wave
+
 template <int BLOCK>
 struct Tile {
-  static constexpr int R = BLOCK / 32;          // row groups
-  static constexpr int NW = 2 * R;              // waves
+  static constexpr int RG = BLOCK / (32 * QT);  // row groups of 32*QT rows
+  static constexpr int NW = 2 * RG;             // waves
   static constexpr int NT = NW * 64;            // threads
   static constexpr int KH = BLOCK / 2;          // keys per wave per block
   static constexpr int KTW = KH / 32;           // 32-key tiles per wave
-  static constexpr int CHUNKS = BLOCK * 16;     // 16-byte chunks per tile
-  static constexpr int LOADS = CHUNKS / NT;     // per thread per tile
-  static constexpr int TILE_BYTES = BLOCK * ROW_BYTES;
-  static_assert(LOADS * NT == CHUNKS, "tile load mapping");
+  static constexpr int SLAB = BLOCK * SLAB_ROW; // bytes per slab
+  static constexpr int BYTES = 4 * SLAB;        // bytes per tile
+  static constexpr int INSTR = BYTES / 1024;    // 1 KiB wave loads per tile
+  static constexpr int LOADS = INSTR / NW;      // per wave per tile
+  static constexpr int IPS = SLAB / 1024;       // wave loads per slab
+  static_assert(LOADS * NW == INSTR, "tile load mapping");
 };
 
-// One LDS stage: K tile then V tile.
+// Issues the direct-to-LDS loads of rows kb*BLOCK .. +BLOCK-1 of one tensor
+// into the tile at LDS byte address `lds`.  Wave load I fills tile bytes
+// 1024*I .. +1023: slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk
+// lane%4, which holds logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).
+// lane_off = (lane/4)*row_bytes + 16*((lane%4) ^ (lane/16)) is the per-lane
+// part of the global byte offset.  Rows at or past N fall outside the buffer
+// resource and read as zeros.  The loads are issued from inline assembly so
+// the compiler does not track them: they are waited for explicitly (vmcnt(0)
+// plus a barrier) one pipeline step later, and no compiler-inserted wait can
+// stall the step in between.
+// One wave load of a tile: rows 16*(I % IPS) + lane/4 of slab I / IPS.
 template <int BLOCK>
-struct Stage {
-  __bf16 k[BLOCK * D];
-  __bf16 v[BLOCK * D];
-};
+__device__ __forceinline__ void issue_load(uint32_t lds, __amdgpu_buffer_rsrc_t rsrc,
+                                           uint32_t lane_off, uint32_t row_bytes,
+                                           int kb, int I) {
+  using TL = Tile<BLOCK>;
+  const uint32_t soff = (uint32_t)kb * BLOCK * row_bytes +
+                        16u * (uint32_t)(I % TL::IPS) * row_bytes +
+                        (uint32_t)(64 * (I / TL::IPS));
+  const uint32_t dst = __builtin_amdgcn_readfirstlane(lds + 1024u * I);
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(dst), "v"(lane_off + soff), "s"(rsrc)
+      : "memory", "m0");
+}
 
-// Issues the direct-to-LDS loads of K and V rows kb*BLOCK .. +BLOCK-1.
-// Load j of wave w fills LDS chunks 64*(w + NW*j) + lane: row (that index)/16,
-// physical chunk lane%16, which holds logical chunk (lane%16) ^ swz(row).
 template <int BLOCK>
-__device__ inline void issue_tile(__bf16* lds_k, __bf16* lds_v,
-                                  __amdgpu_buffer_rsrc_t rk,
-                                  __amdgpu_buffer_rsrc_t rv, int64_t k_row_bytes,
-                                  int64_t v_row_bytes, int kb, int wave,
-                                  int lane) {
+__device__ __forceinline__ void issue_tile(uint32_t lds, __amdgpu_buffer_rsrc_t rsrc,
+                                           uint32_t lane_off, uint32_t row_bytes,
+                                           int kb, int wave) {
   using TL = Tile<BLOCK>;
 #pragma unroll
-  for (int j = 0; j < TL::LOADS; ++j) {
-    const int slot0 = 64 * (wave + TL::NW * j);
-    const int row = (slot0 + lane) / 16;
-    const int chunk = (lane % 16) ^ swz(row);
-    const int grow = kb * BLOCK + row;
-    const uint32_t koff = (uint32_t)(grow * k_row_bytes + chunk * 16);
-    const uint32_t voff = (uint32_t)(grow * v_row_bytes + chunk * 16);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(lds_k + slot0 * 8),
-                                             16, koff, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(lds_v + slot0 * 8),
-                                             16, voff, 0, 0, 0);
+  for (int j = 0; j < TL::LOADS; ++j)
+    issue_load<BLOCK>(lds, rsrc, lane_off, row_bytes, kb, wave + TL::NW * j);
+}
 
+// The loads of one pipeline step: the next K tile and the next V tile, spread
+// over the step's compute so the wave never stalls on issuing them.
+struct StepLoads {
+  uint32_t k_dst, v_dst;          // LDS tile addresses
+  __amdgpu_buffer_rsrc_t rk, rv;
+  uint32_t k_off, v_off;          // per-lane parts of the global offsets
+  uint32_t k_row, v_row;          // row strides in bytes
+  int k_kb, v_kb;                 // key blocks to load
+  int wave;
+};
+
+// Issues load i of the step (i in [0, 2*LOADS): K loads first, then V).
+// Issued unconditionally so the compute region stays one basic block: near
+// the end of a row the key-block indices repeat the last block and the loads
+// land in slots no later step reads.
+template <int BLOCK>
+__device__ __forceinline__ void issue_step_load(const StepLoads& sl, int i) {
+  using TL = Tile<BLOCK>;
+  if (i < TL::LOADS)
+    issue_load<BLOCK>(sl.k_dst, sl.rk, sl.k_off, sl.k_row, sl.k_kb, sl.wave + TL::NW * i);
+  else
+    issue_load<BLOCK>(sl.v_dst, sl.rv, sl.v_off, sl.v_row, sl.v_kb,
+                      sl.wave + TL::NW * (i - TL::LOADS));
+}
+
+__device__ __forceinline__ void wait_loads_and_sync() {
+  __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) expcnt(0) lgkmcnt(0)
+  __syncthreads();
+}
+
+template <int BLOCK>
+struct Scores {
+  f32x16 s[QT][Tile<BLOCK>::KTW];   // [q tile][key tile]
+};
+
+// Per-lane LDS byte offsets (within a tile) of the K and V fragments.
+struct FragAddr {
+  uint32_t k_even, k_odd;   // K rows of this lane, d-steps 2t / 2t+1
+  uint32_t v_lo, v_hi;      // V rows for k-slots 0..3 / 4..7 (transposing read)
+};
+
+template <int BLOCK>
+__device__ __forceinline__ FragAddr frag_addr(int kh, int lane) {
+  using TL = Tile<BLOCK>;
+  const int hl = lane / 32, li = lane % 32;
+  FragAddr f;
+  // K: row KH*kh + 32*kt + li, d = 16*stp + 8*hl: slab stp/2, logical chunk
+  // 2*(stp%2) + hl.  x(row) = (li/4)%4 for every kt.
+  const int krow = TL::KH * kh + li;
+  const int kx = xsw(krow);
+  f.k_even = krow * SLAB_ROW + ((hl ^ kx) * 16);
+  f.k_odd = krow * SLAB_ROW + (((2 + hl) ^ kx) * 16);
+  // V: the transposing read gives lane (group g = lane/16, j = lane%16)
+  // element e of the group's chunk 4e + j/4, entry j%4.  Source lane
+  // sl = 4e + q points at V row (key e of its half: 4*(g/2) + sl/4) and
+  // columns 16*(g%2) + 4q .. +3 of the slab (logical chunk 2*(g%2) + q/2,
+  // byte half q%2).  Rows +8 hold k-slots 4..7.
+  const int g = lane / 16, sl = lane % 16;
+  const int vrow = TL::KH * kh + 4 * (g / 2) + sl / 4;
+  const int lc = 2 * (g % 2) + (sl % 4) / 2;
+  const int half = (sl % 2) * 8;
+  f.v_lo = vrow * SLAB_ROW + ((lc ^ xsw(vrow)) * 16) + half;
+  f.v_hi = (vrow + 8) * SLAB_ROW + ((lc ^ xsw(vrow + 8)) * 16) + half;
+  return f;
+}
+
+// S^T = K Q^T for this wave's keys of one block (K tile at lds_k).
+template <int BLOCK>
+__device__ __forceinline__ void compute_scores(const char* lds_k,
+                                               const bf16x8 (&qf)[QT][8],
+                                               Scores<BLOCK>& sc,
+                                               const FragAddr& fa) {
+  using TL = Tile<BLOCK>;
+#pragma unroll
+  for (int kt = 0; kt < TL::KTW; ++kt) {
+    f32x16 acc[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) acc[qt] = f32x16{};
+#pragma unroll
+    for (int stp = 0; stp < 8; ++stp) {
+      const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) +
+                           (stp / 2) * TL::SLAB + kt * 32 * SLAB_ROW;
+      const bf16x8 a = *(const bf16x8*)(lds_k + off);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+        acc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qt][stp], acc[qt], 0, 0, 0);
+    }
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) sc.s[qt][kt] = acc[qt];
   }
 }
 
 template <int BLOCK>
 struct WaveState {
-  using TL = Tile<BLOCK>;
-  f32x16 o[4];       // O^T tiles: d = 32*dt + C row, query = lane%32
-  float m;           // running max (log2 domain), shared by lanes l, l^32
-  float l;           // partial row sum of this lane's keys
+  f32x16 o[QT][4];   // O^T tiles [q tile][d tile]: d = 32*dt + C row
+  float m[QT];       // running max (log2 domain), shared by lanes l, l^32
+  float l[QT];       // partial row sums of this lane's keys
 };
 
-// Consumes one key block from LDS (K at lds_k, V at lds_v).
+// Keys at or past N (ragged last block) do not exist: their scores become
+// -inf.  `valid` = N - first key of the block.
 template <int BLOCK>
-__device__ inline void consume(const __bf16* lds_k, const __bf16* lds_v,
-                               const bf16x8 (&qf)[8], WaveState<BLOCK>& st,
-                               int kh, int lane, int valid, float scale_log2) {
+__device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int kh, int lane,
+                                          int valid) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
-  const int li = lane % 32;
-  const char* kbase = (const char*)lds_k;
-  const char* vbase = (const char*)lds_v;
-
-  // S^T = K Q^T for this wave's KH keys.
-  f32x16 s[TL::KTW];
-#pragma unroll
-  for (int kt = 0; kt < TL::KTW; ++kt) {
-    const int row = TL::KH * kh + 32 * kt + li;
-    const char* rp = kbase + row * ROW_BYTES;
-    const int sw = swz(row);
-    f32x16 acc = f32x16{};
-#pragma unroll
-    for (int stp = 0; stp < 8; ++stp) {
-      const bf16x8 a = *(const bf16x8*)(rp + (((2 * stp + hl) ^ sw) * 16));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[stp], acc, 0, 0, 0);
-    }
-    s[kt] = acc;
-  }
-
-  // Keys at or past N (ragged last block) do not exist.
   if (valid < BLOCK) {
 #pragma unroll
-    for (int kt = 0; kt < TL::KTW; ++kt)
+    for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = TL::KH * kh + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
-        if (key >= valid) s[kt][r] = -__builtin_inff();
-      }
+      for (int kt = 0; kt < TL::KTW; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = TL::KH * kh + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
+          if (key >= valid) sc.s[qt][kt][r] = -__builtin_inff();
+        }
   }
+}
 
-  float mx = s[0][0];
+template <int BLOCK>
+struct Probs {
+  bf16x8 p[QT][Tile<BLOCK>::KTW][2];   // [q tile][key tile][k-step half]
+  float alpha[QT];
+  float psum[QT];
+  bool raise;
+};
+
+// Rescale of O when a running max was raised, then O^T += V^T P^T (V tile at
+// lds_v).  k-step (kt, c) holds keys 32kt + 16c + {4h..4h+3, 8+4h..8+4h+3},
+// the keys of C registers 8c..8c+7 of S^T tile kt.  Emitted as one chunk per
+// V fragment with the transposing reads issued two fragments ahead, so the
+// LDS latency hides under the MFMAs of the previous fragments.
+template <int BLOCK>
+__device__ __forceinline__ void accumulate_pv(const Probs<BLOCK>& pr,
+                                              const char* lds_v,
+                                              WaveState<BLOCK>& st,
+                                              const FragAddr& fa) {
+  using TL = Tile<BLOCK>;
+  // The test also reads the row sums (never negative, so it does not change
+  // the outcome): this keeps the exponentials ahead of the branch, in the
+  // block where they overlap the next block's score MFMAs.
+  float psum_all = 0.f;
 #pragma unroll
-  for (int kt = 0; kt < TL::KTW; ++kt)
+  for (int qt = 0; qt < QT; ++qt) psum_all += pr.psum[qt];
+  if (__builtin_amdgcn_ballot_w64(pr.raise || !(psum_all >= 0.f))) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
-  mx = pair_max(mx) * scale_log2;
-  const bool raise = mx > st.m + RESCALE_SLACK;
-  if (__builtin_amdgcn_ballot_w64(raise)) {
-    const float alpha = raise ? __builtin_amdgcn_exp2f(st.m - mx) : 1.f;
-    st.m = raise ? mx : st.m;
-    st.l *= alpha;
+    for (int qt = 0; qt < QT; ++qt) {
+      st.l[qt] *= pr.alpha[qt];
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) st.o[dt] *= alpha;
+      for (int dt = 0; dt < 4; ++dt) st.o[qt][dt] *= pr.alpha[qt];
+    }
   }
-  const float m_sub = st.m == -__builtin_inff() ? 0.f : st.m;
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) st.l[qt] += pr.psum[qt];
 
-  // P = exp2(s*scale - m), packed to bf16 in MFMA B-operand order.
-  bf16x8 pf[TL::KTW][2];
-  float psum = 0.f;
+  constexpr int FRAGS = 8 * TL::KTW;   // (kt, c, dt)
+  constexpr int AHEAD = 2;
+  auto vfrag = [&](int f) {
+    const int kt = f / 8, c = (f / 4) % 2, dt = f % 4;
+    const uint32_t off = dt * TL::SLAB + (32 * kt + 16 * c) * SLAB_ROW;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(lds_v + fa.v_lo + off));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(lds_v + fa.v_hi + off));
+    return __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  bf16x8 vf[FRAGS];
 #pragma unroll
-  for (int kt = 0; kt < TL::KTW; ++kt)
+  for (int f = 0; f < AHEAD; ++f) vf[f] = vfrag(f);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+  for (int f = 0; f < FRAGS; ++f) {
+    if (f + AHEAD < FRAGS) vf[f + AHEAD] = vfrag(f + AHEAD);
+    const int kt = f / 8, c = (f / 4) % 2, dt = f % 4;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(
-            __builtin_fmaf(s[kt][8 * c + e], scale_log2, -m_sub));
-        psum += p;
-        pf[kt][c][e] = (__bf16)p;
-      }
-  st.l += psum;
+    for (int qt = 0; qt < QT; ++qt)
+      st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          vf[f], pr.p[qt][kt][c], st.o[qt][dt], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
 
-  // O^T += V^T P^T.  k-step (kt, c) holds keys 32kt + 16c + {4h..4h+3,
-  // 8+4h..8+4h+3} (C registers 8c..8c+7 of S^T tile kt).  The transposing
-  // read gives lane (group g = lane/16, j = lane%16) element e of the 16-lane
-  // group's chunk 4e + j/4, entry j%4, so source lane sl = 4e + q points at
-  // V row (key e of its half) and the 4 columns 4q..4q+3 of its 16-column
-  // group.
-  const int g = lane / 16;
-  const int sl = lane % 16;
-  const int vrow0 = TL::KH * kh + 4 * (g / 2) + sl / 4;
-  const int cb = 2 * (g % 2) + (sl % 4) / 2;
-  const int half = (sl % 2) * 8;
-  const int f0 = swz(vrow0);
-  const int f1 = swz(vrow0 + 8);
+// S(j+1) = K(j+1) Q^T fused with block j's softmax arithmetic.  The MFMAs
+// of the next block do not depend on the softmax of the current one, so the
+// region is emitted as one chunk per MFMA, each carrying a slice of the VALU
+// work, with scheduling barriers between chunks so the compiler keeps the
+// interleave: MFMAs of one wave then run under its own exponentials.
+//   chunks 0..7   row-max slices (4 scores of each q tile per chunk)
+//   chunk  8      row statistics: pair max, raise test, alpha, new max
+//   chunks 8..31  exponentials, row sums and bf16 packing of P (64 scores)
+// K fragments are read two MFMA pairs ahead of their use.
+template <int BLOCK>
+__device__ __forceinline__ void scores_with_softmax(
+    const char* lds_k, const bf16x8 (&qf)[QT][8], Scores<BLOCK>& nxt,
+    const Scores<BLOCK>& cur, WaveState<BLOCK>& st, Probs<BLOCK>& pr,
+    const FragAddr& fa, float scale_log2, const StepLoads& sl) {
+  using TL = Tile<BLOCK>;
+  constexpr int PAIRS = 8 * TL::KTW;      // (key tile, d-step) K fragments
+  constexpr int CHUNKS = QT * PAIRS;      // one MFMA per chunk
+  constexpr int NE = 16 * TL::KTW;        // scores per lane per q tile
+  constexpr int MAX_CHUNKS = CHUNKS / 4;
+  constexpr int EXP_CHUNKS = CHUNKS - MAX_CHUNKS;
+  static_assert(NE % MAX_CHUNKS == 0, "max slices");
+
+  auto kfrag = [&](int pair) {
+    const int kt = pair / 8, stp = pair % 8;
+    const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) +
+                         (stp / 2) * TL::SLAB + kt * 32 * SLAB_ROW;
+    return *(const bf16x8*)(lds_k + off);
+  };
+  auto score = [&](int qt, int e) -> float {   // e: 16*kt + r
+    return cur.s[qt][e / 16][e % 16];
+  };
+  constexpr int AHEAD = 2;                 // K fragments read ahead of use
+
+  bf16x8 kf[PAIRS];
 #pragma unroll
-  for (int kt = 0; kt < TL::KTW; ++kt)
+  for (int i = 0; i < AHEAD; ++i) kf[i] = kfrag(i);
+  float mx[QT], msub[QT], ps[QT];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int row = vrow0 + 32 * kt + 16 * c;
-      const char* r0 = vbase + row * ROW_BYTES + half;
-      const char* r1 = r0 + 8 * ROW_BYTES;
+  for (int t = 0; t < QT; ++t) {
+    mx[t] = -__builtin_inff();
+    msub[t] = 0.f;
+    ps[t] = 0.f;
+  }
+  bool any_raise = false;
+  constexpr int NLOADS = 2 * TL::LOADS;
+  static_assert(CHUNKS % NLOADS == 0, "load spacing");
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        const int pc0 = (4 * dt + cb) ^ f0;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(r0 + pc0 * 16));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(r1 + ((4 * dt + cb) ^ f1) * 16));
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kt][c],
-                                                           st.o[dt], 0, 0, 0);
+  for (int ch = 0; ch < CHUNKS; ++ch) {
+    const int pair = ch / QT, qt = ch % QT;
+    if (ch % (CHUNKS / NLOADS) == 0) issue_step_load<BLOCK>(sl, ch / (CHUNKS / NLOADS));
+    if (qt == 0 && pair + AHEAD < PAIRS) kf[pair + AHEAD] = kfrag(pair + AHEAD);
+    {
+      const int kt = pair / 8, stp = pair % 8;
+      nxt.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          kf[pair], qf[qt][stp], stp == 0 ? f32x16{} : nxt.s[qt][kt], 0, 0, 0);
+    }
+    if (ch < MAX_CHUNKS) {
+      constexpr int W = NE / MAX_CHUNKS;
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int i = 0; i < W; ++i) mx[t] = fmaxf(mx[t], score(t, ch * W + i));
+    }
+    if (ch == MAX_CHUNKS) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const float m = pair_max(mx[t]) * scale_log2;
+        const bool raise = m > st.m[t] + RESCALE_SLACK;
+        const float a = __builtin_amdgcn_exp2f(st.m[t] - m);
+        pr.alpha[t] = raise ? a : 1.f;
+        st.m[t] = raise ? m : st.m[t];
+        any_raise |= raise;
+        msub[t] = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
       }
     }
+    if (ch >= MAX_CHUNKS) {
+      const int e0 = (ch - MAX_CHUNKS) * QT * NE / EXP_CHUNKS;
+      const int e1 = (ch - MAX_CHUNKS + 1) * QT * NE / EXP_CHUNKS;
+#pragma unroll
+      for (int e = e0; e < e1; ++e) {
+        const int t = e / NE, el = e % NE;   // q tile, score index
+        const float p = __builtin_amdgcn_exp2f(
+            __builtin_fmaf(score(t, el), scale_log2, -msub[t]));
+        ps[t] += p;
+        pr.p[t][el / 16][(el % 16) / 8][el % 8] = (__bf16)p;
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int t = 0; t < QT; ++t) pr.psum[t] = ps[t];
+  pr.raise = any_raise;
 }
 
 template <int BLOCK, bool SPARSE>
@@ -258,16 +437,17 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
     float scale_log2) {
   using TL = Tile<BLOCK>;
-  __shared__ __attribute__((aligned(1024))) Stage<BLOCK> st0;
-  __shared__ __attribute__((aligned(1024))) Stage<BLOCK> st1;
+  // Stages: K slots 0-1, V slots 0-2.
+  __shared__ __attribute__((aligned(1024))) char lds[5 * TL::BYTES];
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
 
   const int tid = threadIdx.x;
   const int wave = tid / 64;
   const int lane = tid % 64;
   const int hl = lane / 32;
   const int li = lane % 32;
-  const int rg = wave % TL::R;   // row group
-  const int kh = wave / TL::R;   // key half
+  const int rg = wave % TL::RG;  // row group
+  const int kh = wave / TL::RG;  // key half
 
   const int tile = xcd_remap(blockIdx.x, nb * H);
   const int head = tile / nb;
@@ -279,101 +459,155 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       make_rsrc(kg + head * k_sh, (uint32_t)(((int64_t)(N - 1) * k_st + D) * 2));
   const __amdgpu_buffer_rsrc_t rv =
       make_rsrc(vg + head * v_sh, (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2));
-  const int64_t k_row_bytes = k_st * 2;
-  const int64_t v_row_bytes = v_st * 2;
+  const uint32_t k_row_bytes = (uint32_t)(k_st * 2);
+  const uint32_t v_row_bytes = (uint32_t)(v_st * 2);
+  const uint32_t dma_chunk = 16u * (uint32_t)((lane % 4) ^ (lane / 16));
+  const uint32_t k_lane_off = (uint32_t)(lane / 4) * k_row_bytes + dma_chunk;
+  const uint32_t v_lane_off = (uint32_t)(lane / 4) * v_row_bytes + dma_chunk;
+  const FragAddr fa = frag_addr<BLOCK>(kh, lane);
 
-  // Q fragments: row qrow, k-slots d = 16*stp + 8*hl + 0..7.
-  const int qrow = qb * BLOCK + rg * 32 + li;
-  bf16x8 qf[8];
+  // Q fragments: rows qrow0 + 32*qt, k-slots d = 16*stp + 8*hl + 0..7.
+  const int qrow0 = qb * BLOCK + 32 * QT * rg + li;
+  bf16x8 qf[QT][8];
 #pragma unroll
-  for (int stp = 0; stp < 8; ++stp)
-    qf[stp] = qrow < N ? *(const bf16x8*)(qh + (int64_t)qrow * q_st + 16 * stp + 8 * hl)
-                       : bf16x8{};
-
-  int it = 0, it_end = nb;
-  if constexpr (SPARSE) {
-    it = row_ptr[qb];
-    it_end = row_ptr[qb + 1];
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qrow = qrow0 + 32 * qt;
+#pragma unroll
+    for (int stp = 0; stp < 8; ++stp)
+      qf[qt][stp] = qrow < N
+                        ? *(const bf16x8*)(qh + (int64_t)qrow * q_st + 16 * stp + 8 * hl)
+                        : bf16x8{};
   }
+
+  int beg = 0, n = nb;
+  if constexpr (SPARSE) {
+    beg = row_ptr[qb];
+    n = row_ptr[qb + 1] - beg;
+  }
+  auto kb_at = [&](int j) { return SPARSE ? col_idx[beg + j] : j; };
 
   WaveState<BLOCK> ws;
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt) ws.o[dt] = f32x16{};
-  ws.m = -__builtin_inff();
-  ws.l = 0.f;
+  for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) ws.o[qt][dt] = f32x16{};
+    ws.m[qt] = -__builtin_inff();
+    ws.l[qt] = 0.f;
+  }
 
-  auto kb_at = [&](int i) { return SPARSE ? col_idx[i] : i; };
-  if (it < it_end)
-    issue_tile<BLOCK>(st0.k, st0.v, rk, rv, k_row_bytes, v_row_bytes, kb_at(it),
-                      wave, lane);
+  if (n > 0) {
+    // LDS stages: K(b) in K slot b % 2, V(b) in V slot b % 3.
+    const uint32_t k_slot0 = lds_base, v_slot0 = lds_base + 2 * TL::BYTES;
+    const char* const k_lds = lds;
+    const char* const v_lds = lds + 2 * TL::BYTES;
+    // Key-half-1 waves run one block behind in P V: on each SIMD one wave
+    // exponentiates while the other reads V, which spreads VALU, LDS and
+    // MFMA demand over the whole step.
+    const bool late_pv = false;
 
-  // Two key blocks per trip so that each LDS stage is a distinct object: the
-  // loads into one stage are then known not to alias reads of the other.
-  while (it < it_end) {
-    {
-      const int kb = kb_at(it);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (it + 1 < it_end)
-        issue_tile<BLOCK>(st1.k, st1.v, rk, rv, k_row_bytes, v_row_bytes,
-                          kb_at(it + 1), wave, lane);
-      consume<BLOCK>(st0.k, st0.v, qf, ws, kh, lane, N - kb * BLOCK, scale_log2);
-      ++it;
+    // Prologue: K(0), V(0) resident, S(0) computed, K(1) resident.
+    int kb0 = kb_at(0);
+    int kb1 = n > 1 ? kb_at(1) : kb0;          // block j+1
+    int kb2 = n > 2 ? kb_at(2) : kb1;          // block j+2
+    issue_tile<BLOCK>(k_slot0, rk, k_lane_off, k_row_bytes, kb0, wave);
+    issue_tile<BLOCK>(v_slot0, rv, v_lane_off, v_row_bytes, kb0, wave);
+    wait_loads_and_sync();
+    if (n > 1)
+      issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk, k_lane_off, k_row_bytes, kb1, wave);
+    Scores<BLOCK> sa, sb;
+    compute_scores<BLOCK>(k_lds, qf, sa, fa);
+    mask_tail<BLOCK>(sa, kh, lane, N - kb0 * BLOCK);
+    wait_loads_and_sync();
+
+    Probs<BLOCK> pr;
+    int kslot = 1;   // slot of K(j+1)
+    int vslot = 0;   // slot of V(j)
+    // Step j: S(j) is in `cur`; K(j+1), V(j) (and V(j-1)) are resident.
+    // Load K(j+2) and V(j+1) into the slots step j-1 released, compute S(j+1)
+    // into `nxt`, finish block j (block j-1 for late waves).
+    auto step = [&](int j, Scores<BLOCK>& cur, Scores<BLOCK>& nxt) {
+      const int kb3 = j + 3 < n ? kb_at(j + 3) : kb2;   // scalar load, used next step
+      const int vprev = vslot == 0 ? 2 : vslot - 1;
+      const int vnext = vslot == 2 ? 0 : vslot + 1;
+      const StepLoads sl{k_slot0 + (uint32_t)(1 - kslot) * TL::BYTES,
+                         v_slot0 + (uint32_t)vnext * TL::BYTES, rk, rv,
+                         k_lane_off, v_lane_off, k_row_bytes, v_row_bytes,
+                         kb2, kb1, wave};
+      if (late_pv && j > 0) accumulate_pv<BLOCK>(pr, v_lds + vprev * TL::BYTES, ws, fa);
+      scores_with_softmax<BLOCK>(k_lds + kslot * TL::BYTES, qf, nxt, cur, ws, pr,
+                                 fa, scale_log2, sl);
+      if (!late_pv) accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
+      mask_tail<BLOCK>(nxt, kh, lane, N - kb1 * BLOCK);
+      kb1 = kb2;
+      kb2 = kb3;
+      kslot = 1 - kslot;
+      vslot = vnext;
+      wait_loads_and_sync();
+    };
+    for (int j = 0; j < n; j += 2) {
+      step(j, sa, sb);
+      if (j + 1 >= n) break;
+      step(j + 1, sb, sa);
     }
-    if (it >= it_end) break;
-    {
-      const int kb = kb_at(it);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (it + 1 < it_end)
-        issue_tile<BLOCK>(st0.k, st0.v, rk, rv, k_row_bytes, v_row_bytes,
-                          kb_at(it + 1), wave, lane);
-      consume<BLOCK>(st1.k, st1.v, qf, ws, kh, lane, N - kb * BLOCK, scale_log2);
-      ++it;
+    if (late_pv) {
+      const int vlast = vslot == 0 ? 2 : vslot - 1;
+      accumulate_pv<BLOCK>(pr, v_lds + vlast * TL::BYTES, ws, fa);
     }
+    __syncthreads();
   }
 
   // Merge the two key halves of each row group: the second-half wave leaves
   // its state in LDS (O as [register][lane] floats, conflict-free), the
   // first-half wave combines and stores.
-  __syncthreads();
-  float* mo = (float*)&st0;                 // [R][64 regs][64 lanes]
-  float* mm = (float*)&st1;                 // [R][64 lanes] max
-  float* ml = mm + TL::R * 64;              // [R][64 lanes] pair sums
-  const float lsum = pair_sum(ws.l);
+  float* mo = (float*)lds;                      // [RG][QT*64 regs][64 lanes]
+  float* mm = mo + TL::RG * QT * 64 * 64;       // [RG][QT][64 lanes] max
+  float* ml = mm + TL::RG * QT * 64;            // [RG][QT][64 lanes] pair sums
+  float lsum[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) lsum[qt] = pair_sum(ws.l[qt]);
   if (kh == 1) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mo[(rg * 64 + dt * 16 + r) * 64 + lane] = ws.o[dt][r];
-    mm[rg * 64 + lane] = ws.m;
-    ml[rg * 64 + lane] = lsum;
-  }
-  __syncthreads();
-  if (kh == 0) {
-    const float m1 = mm[rg * 64 + lane];
-    const float l1 = ml[rg * 64 + lane];
-    const float m = fmaxf(ws.m, m1);
-    const float a0 = ws.m == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(ws.m - m);
-    const float a1 = m1 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m1 - m);
-    const float ltot = lsum * a0 + l1 * a1;
-    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-    const float c0 = a0 * inv, c1 = a1 * inv;
-    if (qrow < N) {
-      __bf16* orow = oh + (int64_t)qrow * o_st;
+    for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-          bf16x4 w;
+        for (int r = 0; r < 16; ++r)
+          mo[((rg * QT + qt) * 64 + dt * 16 + r) * 64 + lane] = ws.o[qt][dt][r];
+      mm[(rg * QT + qt) * 64 + lane] = ws.m[qt];
+      ml[(rg * QT + qt) * 64 + lane] = lsum[qt];
+    }
+  }
+  __syncthreads();
+  if (kh == 0) {
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int r = 4 * a + b;
-            w[b] = (__bf16)(ws.o[dt][r] * c0 + mo[(rg * 64 + dt * 16 + r) * 64 + lane] * c1);
+    for (int qt = 0; qt < QT; ++qt) {
+      const float m1 = mm[(rg * QT + qt) * 64 + lane];
+      const float l1 = ml[(rg * QT + qt) * 64 + lane];
+      const float m0 = ws.m[qt];
+      const float m = fmaxf(m0, m1);
+      const float a0 = m0 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m0 - m);
+      const float a1 = m1 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m1 - m);
+      const float ltot = lsum[qt] * a0 + l1 * a1;
+      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+      const float c0 = a0 * inv, c1 = a1 * inv;
+      const int qrow = qrow0 + 32 * qt;
+      if (qrow < N) {
+        __bf16* orow = oh + (int64_t)qrow * o_st;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+            bf16x4 w;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int r = 4 * a + b;
+              w[b] = (__bf16)(ws.o[qt][dt][r] * c0 +
+                              mo[((rg * QT + qt) * 64 + dt * 16 + r) * 64 + lane] * c1);
+            }
+            *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
           }
-          *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
-        }
+      }
     }
   }
 }
