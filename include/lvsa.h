@@ -44,7 +44,7 @@ typedef int32_t lvsa_status;
 #define LVSA_EINVAL (-1)        /* an argument is out of range or inconsistent */
 #define LVSA_ENOMEM (-2)        /* host or device allocation failed            */
 #define LVSA_EDEVICE (-3)       /* a HIP runtime call or kernel launch failed  */
-#define LVSA_EUNSUPPORTED (-4)  /* valid, but not a shape/layout this build has */
+#define LVSA_EUNSUPPORTED (-4)  /* valid, but a shape or layout not implemented */
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* lvsa_status_str(lvsa_status s);
