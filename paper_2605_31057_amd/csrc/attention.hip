@@ -43,6 +43,7 @@ namespace lvsa {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -123,57 +124,90 @@ struct Tile {
 // the compiler does not track them: they are waited for explicitly (vmcnt(0)
 // plus a barrier) one pipeline step later, and no compiler-inserted wait can
 // stall the step in between.
-// One wave load of a tile: rows 16*(I % IPS) + lane/4 of slab I / IPS.
-template <int BLOCK>
-__device__ __forceinline__ void issue_load(uint32_t lds, __amdgpu_buffer_rsrc_t rsrc,
-                                           uint32_t lane_off, uint32_t row_bytes,
-                                           int kb, int I) {
-  using TL = Tile<BLOCK>;
-  const uint32_t soff = (uint32_t)kb * BLOCK * row_bytes +
-                        16u * (uint32_t)(I % TL::IPS) * row_bytes +
-                        (uint32_t)(64 * (I / TL::IPS));
-  const uint32_t dst = __builtin_amdgcn_readfirstlane(lds + 1024u * I);
+// One wave load of a tile into LDS bytes 1024*I ..: `rsrc` starts at the
+// tile's first row, `voff` = per-lane offset + the load's uniform offset.
+__device__ __forceinline__ void issue_load(uint32_t lds_dst, __amdgpu_buffer_rsrc_t rsrc,
+                                           uint32_t voff) {
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
       "buffer_load_dwordx4 %1, %2, 0 offen lds"
       :
-      : "s"(dst), "v"(lane_off + soff), "s"(rsrc)
+      : "s"(lds_dst), "v"(voff), "s"(rsrc)
       : "memory", "m0");
+}
+
+// Buffer resource over rows kb*BLOCK .. N-1 of one head of K or V; a key
+// block index outside [0, nb) yields an empty resource (all loads read 0).
+template <int BLOCK>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const __bf16* head_base,
+                                                            int64_t row_elems,
+                                                            uint32_t head_bytes,
+                                                            int kb, int nb) {
+  const bool ok = (uint32_t)kb < (uint32_t)nb;
+  const int64_t skip = ok ? (int64_t)kb * BLOCK * row_elems : 0;
+  const uint32_t bytes = ok ? head_bytes - (uint32_t)(skip * 2) : 0u;
+  return make_rsrc(head_base + skip, bytes);
+}
+
+// Per-wave load plan: load j of wave w fills tile bytes 1024*I (I = w + NW*j):
+// slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk lane%4, which holds
+// logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).  The per-lane part
+// of the global offset is (lane/4)*row_bytes + 16*((lane%4) ^ (lane/16)); the
+// per-load part is uniform.
+template <int BLOCK>
+struct LoadPlan {
+  uint32_t lane_off;
+  uint32_t part[Tile<BLOCK>::LOADS];
+  uint32_t lds_part[Tile<BLOCK>::LOADS];
+};
+
+template <int BLOCK>
+__device__ __forceinline__ LoadPlan<BLOCK> load_plan(uint32_t row_bytes, int wave,
+                                                     int lane) {
+  using TL = Tile<BLOCK>;
+  LoadPlan<BLOCK> lp;
+  lp.lane_off = (uint32_t)(lane / 4) * row_bytes +
+                16u * (uint32_t)((lane % 4) ^ (lane / 16));
+#pragma unroll
+  for (int j = 0; j < TL::LOADS; ++j) {
+    const int I = wave + TL::NW * j;
+    lp.part[j] = (uint32_t)__builtin_amdgcn_readfirstlane(
+        16u * (uint32_t)(I % TL::IPS) * row_bytes + (uint32_t)(64 * (I / TL::IPS)));
+    lp.lds_part[j] = (uint32_t)__builtin_amdgcn_readfirstlane(1024u * (uint32_t)I);
+  }
+  return lp;
 }
 
 template <int BLOCK>
 __device__ __forceinline__ void issue_tile(uint32_t lds, __amdgpu_buffer_rsrc_t rsrc,
-                                           uint32_t lane_off, uint32_t row_bytes,
-                                           int kb, int wave) {
+                                           const LoadPlan<BLOCK>& lp) {
   using TL = Tile<BLOCK>;
 #pragma unroll
   for (int j = 0; j < TL::LOADS; ++j)
-    issue_load<BLOCK>(lds, rsrc, lane_off, row_bytes, kb, wave + TL::NW * j);
+    issue_load(lds + lp.lds_part[j], rsrc, lp.lane_off + lp.part[j]);
 }
 
 // The loads of one pipeline step: the next K tile and the next V tile, spread
-// over the step's compute so the wave never stalls on issuing them.
+// over the step's compute so the wave never stalls on issuing them.  Issued
+// unconditionally so the compute region stays one basic block: near the end
+// of a row the key-block indices repeat the last block and the loads land in
+// slots no later step reads.
+template <int BLOCK>
 struct StepLoads {
-  uint32_t k_dst, v_dst;          // LDS tile addresses
-  __amdgpu_buffer_rsrc_t rk, rv;
-  uint32_t k_off, v_off;          // per-lane parts of the global offsets
-  uint32_t k_row, v_row;          // row strides in bytes
-  int k_kb, v_kb;                 // key blocks to load
-  int wave;
+  uint32_t k_dst, v_dst;                 // LDS tile addresses
+  __amdgpu_buffer_rsrc_t rk, rv;         // resources starting at the tiles
+  const LoadPlan<BLOCK>* kp;
+  const LoadPlan<BLOCK>* vp;
 };
 
-// Issues load i of the step (i in [0, 2*LOADS): K loads first, then V).
-// Issued unconditionally so the compute region stays one basic block: near
-// the end of a row the key-block indices repeat the last block and the loads
-// land in slots no later step reads.
 template <int BLOCK>
-__device__ __forceinline__ void issue_step_load(const StepLoads& sl, int i) {
+__device__ __forceinline__ void issue_step_load(const StepLoads<BLOCK>& sl, int i) {
   using TL = Tile<BLOCK>;
   if (i < TL::LOADS)
-    issue_load<BLOCK>(sl.k_dst, sl.rk, sl.k_off, sl.k_row, sl.k_kb, sl.wave + TL::NW * i);
+    issue_load(sl.k_dst + sl.kp->lds_part[i], sl.rk, sl.kp->lane_off + sl.kp->part[i]);
   else
-    issue_load<BLOCK>(sl.v_dst, sl.rv, sl.v_off, sl.v_row, sl.v_kb,
-                      sl.wave + TL::NW * (i - TL::LOADS));
+    issue_load(sl.v_dst + sl.vp->lds_part[i - TL::LOADS], sl.rv,
+               sl.vp->lane_off + sl.vp->part[i - TL::LOADS]);
 }
 
 __device__ __forceinline__ void wait_loads_and_sync() {
@@ -347,7 +381,7 @@ template <int BLOCK>
 __device__ __forceinline__ void scores_with_softmax(
     const char* lds_k, const bf16x8 (&qf)[QT][8], Scores<BLOCK>& nxt,
     const Scores<BLOCK>& cur, WaveState<BLOCK>& st, Probs<BLOCK>& pr,
-    const FragAddr& fa, float scale_log2, const StepLoads& sl) {
+    const FragAddr& fa, float scale_log2, const StepLoads<BLOCK>& sl) {
   using TL = Tile<BLOCK>;
   constexpr int PAIRS = 8 * TL::KTW;      // (key tile, d-step) K fragments
   constexpr int CHUNKS = QT * PAIRS;      // one MFMA per chunk
@@ -410,15 +444,23 @@ __device__ __forceinline__ void scores_with_softmax(
       }
     }
     if (ch >= MAX_CHUNKS) {
-      const int e0 = (ch - MAX_CHUNKS) * QT * NE / EXP_CHUNKS;
-      const int e1 = (ch - MAX_CHUNKS + 1) * QT * NE / EXP_CHUNKS;
+      // P in pairs: exponentials, bf16 packing, and the row sum of the
+      // packed values with one dot2 per pair (the sum matches what P.V sees).
+      constexpr int NP = QT * NE / 2;
+      const int p0 = (ch - MAX_CHUNKS) * NP / EXP_CHUNKS;
+      const int p1 = (ch - MAX_CHUNKS + 1) * NP / EXP_CHUNKS;
 #pragma unroll
-      for (int e = e0; e < e1; ++e) {
-        const int t = e / NE, el = e % NE;   // q tile, score index
-        const float p = __builtin_amdgcn_exp2f(
+      for (int pi = p0; pi < p1; ++pi) {
+        const int t = (2 * pi) / NE, el = (2 * pi) % NE;   // q tile, score index
+        const float a = __builtin_amdgcn_exp2f(
             __builtin_fmaf(score(t, el), scale_log2, -msub[t]));
-        ps[t] += p;
-        pr.p[t][el / 16][(el % 16) / 8][el % 8] = (__bf16)p;
+        const float b = __builtin_amdgcn_exp2f(
+            __builtin_fmaf(score(t, el + 1), scale_log2, -msub[t]));
+        const bf16x2 pk = {(__bf16)a, (__bf16)b};
+        ps[t] = __builtin_amdgcn_fdot2_f32_bf16(pk, bf16x2{(__bf16)1.f, (__bf16)1.f},
+                                                ps[t], false);
+        pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
+        pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
       }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -455,15 +497,14 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
 
   const __bf16* qh = qg + head * q_sh;
   __bf16* oh = og + head * o_sh;
-  const __amdgpu_buffer_rsrc_t rk =
-      make_rsrc(kg + head * k_sh, (uint32_t)(((int64_t)(N - 1) * k_st + D) * 2));
-  const __amdgpu_buffer_rsrc_t rv =
-      make_rsrc(vg + head * v_sh, (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2));
-  const uint32_t k_row_bytes = (uint32_t)(k_st * 2);
-  const uint32_t v_row_bytes = (uint32_t)(v_st * 2);
-  const uint32_t dma_chunk = 16u * (uint32_t)((lane % 4) ^ (lane / 16));
-  const uint32_t k_lane_off = (uint32_t)(lane / 4) * k_row_bytes + dma_chunk;
-  const uint32_t v_lane_off = (uint32_t)(lane / 4) * v_row_bytes + dma_chunk;
+  const __bf16* const kh_base = kg + head * k_sh;
+  const __bf16* const vh_base = vg + head * v_sh;
+  const uint32_t k_bytes = (uint32_t)(((int64_t)(N - 1) * k_st + D) * 2);
+  const uint32_t v_bytes = (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2);
+  const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
+  const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
+  auto rk_at = [&](int kb) { return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, kb, nb); };
+  auto rv_at = [&](int kb) { return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, kb, nb); };
   const FragAddr fa = frag_addr<BLOCK>(kh, lane);
 
   // Q fragments: rows qrow0 + 32*qt, k-slots d = 16*stp + 8*hl + 0..7.
@@ -485,6 +526,16 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     n = row_ptr[qb + 1] - beg;
   }
   auto kb_at = [&](int j) { return SPARSE ? col_idx[beg + j] : j; };
+  // Key block j+3 is fetched by a vector load one step before it is needed,
+  // so the load's latency hides under a whole step (a scalar load would be
+  // waited for at the next LDS wait, which shares its counter).
+  const __amdgpu_buffer_rsrc_t rci =
+      make_rsrc(col_idx, SPARSE ? (uint32_t)(row_ptr[nb] * 4) : 0u);
+  auto kb_fetch = [&](int j) -> int {   // VGPR value, clamped to the row
+    if constexpr (!SPARSE) return j < n ? j : n - 1;
+    const int jj = j < n ? j : n - 1;
+    return __builtin_amdgcn_raw_buffer_load_b32(rci, (beg + jj) * 4, 0, 0);
+  };
 
   WaveState<BLOCK> ws;
 #pragma unroll
@@ -509,11 +560,10 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     int kb0 = kb_at(0);
     int kb1 = n > 1 ? kb_at(1) : kb0;          // block j+1
     int kb2 = n > 2 ? kb_at(2) : kb1;          // block j+2
-    issue_tile<BLOCK>(k_slot0, rk, k_lane_off, k_row_bytes, kb0, wave);
-    issue_tile<BLOCK>(v_slot0, rv, v_lane_off, v_row_bytes, kb0, wave);
+    issue_tile<BLOCK>(k_slot0, rk_at(kb0), kp);
+    issue_tile<BLOCK>(v_slot0, rv_at(kb0), vp);
     wait_loads_and_sync();
-    if (n > 1)
-      issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk, k_lane_off, k_row_bytes, kb1, wave);
+    if (n > 1) issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(kb1), kp);
     Scores<BLOCK> sa, sb;
     compute_scores<BLOCK>(k_lds, qf, sa, fa);
     mask_tail<BLOCK>(sa, kh, lane, N - kb0 * BLOCK);
@@ -526,23 +576,23 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     // Load K(j+2) and V(j+1) into the slots step j-1 released, compute S(j+1)
     // into `nxt`, finish block j (block j-1 for late waves).
     auto step = [&](int j, Scores<BLOCK>& cur, Scores<BLOCK>& nxt) {
-      const int kb3 = j + 3 < n ? kb_at(j + 3) : kb2;   // scalar load, used next step
+      const int kb3v = kb_fetch(j + 3);          // consumed after the barrier
       const int vprev = vslot == 0 ? 2 : vslot - 1;
       const int vnext = vslot == 2 ? 0 : vslot + 1;
-      const StepLoads sl{k_slot0 + (uint32_t)(1 - kslot) * TL::BYTES,
-                         v_slot0 + (uint32_t)vnext * TL::BYTES, rk, rv,
-                         k_lane_off, v_lane_off, k_row_bytes, v_row_bytes,
-                         kb2, kb1, wave};
+      const StepLoads<BLOCK> sl{
+          (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(1 - kslot) * TL::BYTES),
+          (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)vnext * TL::BYTES),
+          rk_at(kb2), rv_at(kb1), &kp, &vp};
       if (late_pv && j > 0) accumulate_pv<BLOCK>(pr, v_lds + vprev * TL::BYTES, ws, fa);
       scores_with_softmax<BLOCK>(k_lds + kslot * TL::BYTES, qf, nxt, cur, ws, pr,
                                  fa, scale_log2, sl);
       if (!late_pv) accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
       mask_tail<BLOCK>(nxt, kh, lane, N - kb1 * BLOCK);
-      kb1 = kb2;
-      kb2 = kb3;
       kslot = 1 - kslot;
       vslot = vnext;
       wait_loads_and_sync();
+      kb1 = kb2;
+      kb2 = __builtin_amdgcn_readfirstlane(kb3v);
     };
     for (int j = 0; j < n; j += 2) {
       step(j, sa, sb);
