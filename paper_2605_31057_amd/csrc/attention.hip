@@ -5,15 +5,15 @@
 // (all keys) with the same kernel visiting every key block.
 //
 // Work decomposition
-//   One workgroup per (head, query block of BLOCK rows); 2*BLOCK/64 waves, one
-//   per SIMD at BLOCK = 128.  Wave w owns 64 query rows (row group w % RG, as
-//   two 32-row MFMA tiles) and one half of the keys of every key block
-//   (w / RG).  The two waves of a row group keep independent online softmax
-//   states over disjoint keys and are merged once at the end.  Holding 64 rows
-//   per wave lets every K and V fragment read from LDS feed two MFMAs.
+//   One workgroup per (head, query block of BLOCK rows) with 2*BLOCK/(32*QT)
+//   waves: 8 waves (two per SIMD) at BLOCK = 128 and QT = 1.  Wave w owns
+//   32*QT query rows (row group w % RG, as QT 32-row MFMA tiles) and one half
+//   of the keys of every key block (w / RG).  The two waves of a row group
+//   keep independent online softmax states over disjoint keys and are merged
+//   once at the end.
 //
 // Pipeline (per wave, one key block per step)
-//   LDS holds two K stages and two V stages (slab layout, see below).  K runs one block ahead of V:
+//   LDS holds two K stages and three V stages (slab layout, see below).  K runs one block ahead of V:
 //   during step j the wave computes S(j+1) = K(j+1) Q^T while it exponentiates
 //   S(j) and accumulates P(j) V(j), so MFMA and VALU work of one wave overlap;
 //   meanwhile K(j+2) and V(j+1) stream from HBM/L2 into the free stages with
@@ -126,10 +126,13 @@ struct Tile {
 // stall the step in between.
 // One wave load of a tile into LDS bytes 1024*I ..: `rsrc` starts at the
 // tile's first row, `voff` = per-lane offset + the load's uniform offset.
+// The nop is the wait state gfx9 needs between an SALU write of M0 and an
+// LDS-DMA instruction (the compiler cannot see into the statement to add it).
 __device__ __forceinline__ void issue_load(uint32_t lds_dst, __amdgpu_buffer_rsrc_t rsrc,
                                            uint32_t voff) {
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
       "buffer_load_dwordx4 %1, %2, 0 offen lds"
       :
       : "s"(lds_dst), "v"(voff), "s"(rsrc)
@@ -551,10 +554,6 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const uint32_t k_slot0 = lds_base, v_slot0 = lds_base + 2 * TL::BYTES;
     const char* const k_lds = lds;
     const char* const v_lds = lds + 2 * TL::BYTES;
-    // Key-half-1 waves run one block behind in P V: on each SIMD one wave
-    // exponentiates while the other reads V, which spreads VALU, LDS and
-    // MFMA demand over the whole step.
-    const bool late_pv = false;
 
     // Prologue: K(0), V(0) resident, S(0) computed, K(1) resident.
     int kb0 = kb_at(0);
@@ -574,19 +573,17 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     int vslot = 0;   // slot of V(j)
     // Step j: S(j) is in `cur`; K(j+1), V(j) (and V(j-1)) are resident.
     // Load K(j+2) and V(j+1) into the slots step j-1 released, compute S(j+1)
-    // into `nxt`, finish block j (block j-1 for late waves).
+    // into `nxt`, finish block j.
     auto step = [&](int j, Scores<BLOCK>& cur, Scores<BLOCK>& nxt) {
       const int kb3v = kb_fetch(j + 3);          // consumed after the barrier
-      const int vprev = vslot == 0 ? 2 : vslot - 1;
       const int vnext = vslot == 2 ? 0 : vslot + 1;
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(1 - kslot) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)vnext * TL::BYTES),
           rk_at(kb2), rv_at(kb1), &kp, &vp};
-      if (late_pv && j > 0) accumulate_pv<BLOCK>(pr, v_lds + vprev * TL::BYTES, ws, fa);
       scores_with_softmax<BLOCK>(k_lds + kslot * TL::BYTES, qf, nxt, cur, ws, pr,
                                  fa, scale_log2, sl);
-      if (!late_pv) accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
+      accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
       mask_tail<BLOCK>(nxt, kh, lane, N - kb1 * BLOCK);
       kslot = 1 - kslot;
       vslot = vnext;
@@ -598,10 +595,6 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       step(j, sa, sb);
       if (j + 1 >= n) break;
       step(j + 1, sb, sa);
-    }
-    if (late_pv) {
-      const int vlast = vslot == 0 ? 2 : vslot - 1;
-      accumulate_pv<BLOCK>(pr, v_lds + vlast * TL::BYTES, ws, fa);
     }
     __syncthreads();
   }
