@@ -7,9 +7,10 @@ with the library under ``paper_2605_31057_amd/`` and imports nothing from it.
 What is computed (LVSA paper, Sec. 2):
   * Eq. 1 (dense):  Attn(q_i) = sum_j softmax_j(q_i . k_j / sqrt(d)) v_j over
     all N keys.
-  * Eq. 2 (sparse): the same softmax restricted to a key set.  ``mode="block"``
-    takes, for every query of query block qb, the keys of the kept key blocks
-    of qb (the CSR the mask oracle emits); ``mode="frame"`` takes the keys whose
+  * Eq. 2 (sparse): the same softmax restricted to a key set.
+    ``block_sparse_attention`` takes, for every query of query block qb, the
+    keys of the kept key blocks of qb (the CSR the mask oracle emits);
+    ``frame_sparse_attention`` and ``frame_sparse_rows`` take the keys whose
     frame is in A(frame of the query), which is Eq. 2 token for token.
 
 Plain numpy: one matrix product for the logits, the textbook max-shifted
@@ -94,6 +95,25 @@ def frame_sparse_attention(q, k, v, A, P, dtype=np.float32):
             out[h, rows] = attend(np.asarray(q[h, rows], dtype=dtype),
                                   np.asarray(k[h, keys], dtype=dtype),
                                   np.asarray(v[h, keys], dtype=dtype))
+    return out
+
+
+def frame_sparse_rows(q, k, v, A, P, heads, rows, dtype=np.float32):
+    """Eq. 2 token for token on selected query rows (rows are independent).
+
+    q, k, v: [H, N, d]; A: list of frame sets; heads, rows: the heads and
+    query token indices to evaluate.  Returns {h: [len(rows), d]}.
+    """
+    out = {}
+    for h in heads:
+        res = []
+        for i in rows:
+            keys = np.concatenate([np.arange(tau * P, (tau + 1) * P)
+                                   for tau in sorted(A[i // P])])
+            res.append(attend(np.asarray(q[h, i:i + 1], dtype=dtype),
+                              np.asarray(k[h, keys], dtype=dtype),
+                              np.asarray(v[h, keys], dtype=dtype))[0])
+        out[h] = np.stack(res)
     return out
 
 

@@ -140,6 +140,17 @@ def frame_mask(A, T):
     return [[1 if tau in A[t] else 0 for tau in range(T)] for t in range(T)]
 
 
+def token_mask(A, T, P):
+    """Eq. 2 at token granularity as an N x N numpy bool array.
+
+    Entry (i, j) is True iff key token j's frame j // P is in A(i // P): the
+    frame mask with every entry repeated over a P x P tile of tokens.
+    """
+    import numpy as np
+    return np.kron(np.array(frame_mask(A, T), dtype=bool),
+                   np.ones((P, P), dtype=bool))
+
+
 def block_keep_bruteforce(A, T, P, B):
     """Kept (q-block, kv-block) pairs by brute force over token pairs.
 

@@ -265,3 +265,40 @@ def test_large_config_counts():
 def test_invalid_budget_rejected():
     with pytest.raises(ValueError):
         M.anchor_period(30, 13, 6)
+
+
+# ------------------------------------------------------- token level ---
+
+@pytest.mark.parametrize("T,P,s,W,tper", [(4, 3, 0, 0, 4), (5, 7, 2, 1, 2),
+                                           (6, 5, 3, 1, 3), (9, 2, 4, 2, 4)])
+def test_token_mask_is_eq2_elementwise(T, P, s, W, tper):
+    """Eq. 2 at token level: (i, j) kept iff frame(j) in A(frame(i)), checked
+    element by element from integer division, and each frame-pair tile of
+    the matrix is constant."""
+    _, _, A = M.attended_frames(T, s, W=W, tper=tper)
+    tm = M.token_mask(A, T, P)
+    N = T * P
+    assert tm.shape == (N, N)
+    for i in range(N):
+        for j in range(N):
+            assert bool(tm[i, j]) == ((j // P) in A[i // P]), (i, j)
+    # Every query token keeps its own frame (t in A(t)), so no row is empty.
+    assert tm.any(axis=1).all()
+    assert all(tm[i, i] for i in range(N))
+
+
+@pytest.mark.parametrize("T,P,B", [(5, 7, 4), (6, 5, 3), (4, 6, 4), (7, 3, 2)])
+def test_block_rule_is_smallest_cover_of_token_mask(T, P, B):
+    """The any-overlap block rule keeps exactly the blocks that hold at least
+    one Eq. 2 token pair: a superset of the token mask with no empty block."""
+    for s in range(3):
+        _, _, A = M.attended_frames(T, s, W=1, tper=3)
+        tm = M.token_mask(A, T, P)
+        N = T * P
+        nb = M.ceil_div(N, B)
+        row_ptr, col_idx = M.to_csr(M.block_keep(A, T, P, B))
+        for qb in range(nb):
+            kept = set(col_idx[row_ptr[qb]:row_ptr[qb + 1]])
+            for kb in range(nb):
+                tile = tm[qb * B:min((qb + 1) * B, N), kb * B:min((kb + 1) * B, N)]
+                assert (kb in kept) == bool(tile.any()), (s, qb, kb)
