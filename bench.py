@@ -9,8 +9,9 @@ C = 21, W = 6).  Successive steps sweep s = 0, 1, 2, ... so the anchors
 rotate as in a denoising loop.  Inputs are resident in HBM before timing.
 
 Prints ONE JSON line.  Besides the step throughput it reports the attention
-call alone (hipEvents), the dense kernel of the same design, the roofline
-position of the sparse kernel, and the CPU oracle on a bounded sample.
+call alone (hipEvents), the token-exact form of the same mask (Eq. 2 token
+for token), the dense kernel of the same design, the roofline position of the
+sparse kernel, and the CPU oracle on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload wan13_6x]
 """
@@ -226,6 +227,40 @@ def main():
         stream=stream), 20, 3)
     print(f"[bench] attention {attn_med:.3f} ms", file=sys.stderr, flush=True)
 
+    # Token-exact form (Eq. 2 token for token) at the same step: the same
+    # kept blocks, with frame-edge parts of straddling blocks masked.
+    ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    exact = {}
+    try:
+        me = L.build_exact_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref,
+                                       rp, ent, params=params, stream=stream)
+    except L.LvsaError:
+        me = None
+    if me is not None:
+        ex_med = median(time_calls(
+            lambda: L.attention_exact(q, k, v, me, out=out, stream=stream), 20, 3))
+        _, anc, lo, hi = L.frame_sets(w.frames, s_ref, params)
+        per_frame = [len(set(anc) | set(range(lo[t], hi[t] + 1)))
+                     for t in range(w.frames)]
+        eq2_flops = 4.0 * 128 * w.heads * w.tokens_per_frame ** 2 * sum(per_frame)
+        host_ex = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            L.build_mask(w.frames, w.tokens_per_frame, w.block, s_ref, params,
+                         exact=True).free()
+            host_ex.append((time.perf_counter() - t0) * 1e6)
+        exact = {
+            "exact_ms_per_call": ex_med,
+            "exact_mask_build_host_us": median(host_ex),
+            "exact_tflops_eq2_pairs": eq2_flops / (ex_med * 1e-3) / 1e12,
+            "exact_vs_block_time": ex_med / attn_med,
+            "token_density_step10": eq2_flops / (4.0 * 128 * w.heads * w.n_tokens ** 2),
+        }
+        print(f"[bench] exact attention {ex_med:.3f} ms", file=sys.stderr, flush=True)
+        # The block form again, for the step loop's mask buffers.
+        m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
+                                params=params, stream=stream)
+
     dense = {}
     if not args.no_dense:
         print("[bench] dense", file=sys.stderr, flush=True)
@@ -270,6 +305,7 @@ def main():
         "mask_build_host_us": median(host_us),
         "nnz_step10": nnz_of[s_ref],
         "block_density_step10": nnz_of[s_ref] / (nb * nb),
+        **exact,
         **dense,
         "roofline": {
             "kernel": "attn_fwd_kernel<128, sparse>",

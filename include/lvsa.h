@@ -132,8 +132,9 @@ lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
                           int32_t* block, int32_t* n_blocks, int64_t* nnz,
                           const int32_t** row_ptr, const int32_t** col_idx);
 
-/* Copies the host arrays to device memory owned by the handle (allocated on
- * the first call, on the current device), asynchronously on `stream`; the
+/* Copies the host arrays (and the token-exact entry words, when the handle
+ * has them) to device memory owned by the handle (allocated on the first
+ * call, on the current device), asynchronously on `stream`; the
  * host arrays must stay unmodified until the stream reaches the copy, which
  * lvsa_csr_free respects by synchronizing the device before releasing.
  * Errors: EINVAL (null), ENOMEM, EDEVICE. */
@@ -169,6 +170,65 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t* d_col_idx, int64_t col_capacity,
                                    void* stream);
 
+/* ------------------------------------------------ token-exact form ---- */
+
+/* When B does not divide P, a block can straddle a frame edge and the block
+ * rule above keeps some token pairs that Eq. 2 drops.  The token-exact form
+ * keeps the same blocks (same row_ptr, same order) and gives every kept block
+ * an entry word that says which of its query-frame / key-frame parts are
+ * attended, so attention computes Eq. 2 token for token (Sec. 2, Eq. 2).
+ * It needs P >= B (a block then touches at most two frames), B <= 255 and
+ * nb <= 65536.
+ *
+ * Entry word (uint32) of kept pair (qb, kb); f0 <= f1 are the frames touched
+ * by qb, g0 <= g1 those touched by kb (equal when the block lies in one frame):
+ *   bits  0..15  kb
+ *   bits 16..23  kfirst: tokens of kb in frame g0 (B when g0 == g1)
+ *   bits 24..27  pattern: bit 2a+b set iff frame (b ? g1 : g0) is in
+ *                A(a ? f1 : f0)
+ *   bits 28..31  zero
+ * Query token i of qb attends key token j of kb iff pattern bit
+ * 2*(frame(i) != f0) + (frame(j) != g0) is set. */
+typedef struct lvsa_exact_mask {
+  int32_t n_tokens;        /* N = T*P                                       */
+  int32_t block;           /* B                                             */
+  int32_t n_blocks;        /* nb = ceil(N / B)                              */
+  int32_t frame_tokens;    /* P >= B                                        */
+  const int32_t* row_ptr;  /* device, [nb + 1], as in lvsa_block_mask       */
+  const uint32_t* entry;   /* device, [row_ptr[nb]] entry words, kb ascending */
+} lvsa_exact_mask;
+
+/* Host builder of the token-exact form: the handle of lvsa_build_mask
+ * (same arguments, same row_ptr and col_idx) plus one entry word per kept
+ * block.  Errors as for lvsa_build_mask, and EUNSUPPORTED when P < B,
+ * B > 255 or nb > 65536.  *out is set to NULL on error. */
+lvsa_status lvsa_build_exact_mask(int32_t T, int32_t P, int32_t B,
+                                  int32_t step, int32_t layer,
+                                  const lvsa_params* p, lvsa_csr** out);
+
+/* Host entry words of a handle built by lvsa_build_exact_mask (valid until
+ * lvsa_csr_free; nnz of them) and its P.  Errors: EINVAL (null),
+ * EUNSUPPORTED for a handle without entry words (lvsa_build_mask). */
+lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
+                             const uint32_t** entry);
+
+/* Device view of the token-exact form of an uploaded handle built by
+ * lvsa_build_exact_mask (lvsa_csr_upload copies the entry words too).
+ * Errors: EINVAL if never uploaded, EUNSUPPORTED as for lvsa_csr_entries. */
+lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out);
+
+/* Device builder of the token-exact form: row_ptr and entry words of the
+ * same mask as lvsa_build_mask_device, on `stream`, into caller-owned buffers
+ *   d_row_ptr  device int32[nb + 1]
+ *   d_entry    device uint32[entry_capacity], entry_capacity >= nb * nb
+ * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED (P < B, B > 255,
+ * nb > 65536), EDEVICE (launch). */
+lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
+                                         int32_t step, int32_t layer,
+                                         const lvsa_params* p,
+                                         int32_t* d_row_ptr, uint32_t* d_entry,
+                                         int64_t entry_capacity, void* stream);
+
 /* --------------------------------------------------------- attention ---- */
 
 /* A bf16 tensor [heads, n_tokens, head_dim] in device memory.  Element
@@ -197,6 +257,17 @@ typedef struct lvsa_tensor {
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream);
+
+/* Token-exact attention forward (Eq. 2 token for token): as lvsa_attention,
+ * with the keys of each kept block further restricted, per query token, by
+ * the block's entry word, so query i attends exactly the keys j with
+ * frame(j) in A(frame(i)).  mask->block is 64 or 128 and mask->frame_tokens
+ * >= mask->block; every query token keeps at least its own frame's keys.
+ * Errors as for lvsa_attention. */
+lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
+                                 const lvsa_tensor* v,
+                                 const lvsa_exact_mask* mask, lvsa_tensor* out,
+                                 void* stream);
 
 /* Dense attention forward (Eq. 1 over all N keys), the same kernel design
  * visiting every key block; `block` (64 or 128) is its tile size.

@@ -11,13 +11,17 @@ fallback.
     csr = lvsa.build_mask(T=121, P=1560, B=128, step=10, params=p)
     csr.upload()
     lvsa.attention(q, k, v, csr.device_mask(), out)      # q,k,v,out: [H,N,128] bf16
+    ex = lvsa.build_mask(T=121, P=1560, B=128, step=10, params=p, exact=True)
+    ex.upload()
+    lvsa.attention_exact(q, k, v, ex.exact_mask(), out)  # Eq. 2 token for token
 """
 import ctypes
 import os
 
 __all__ = [
-    "LvsaError", "Params", "Csr", "BlockMask", "lib", "params_default",
-    "frame_sets", "build_mask", "build_mask_device", "attention",
+    "LvsaError", "Params", "Csr", "BlockMask", "ExactMask", "lib",
+    "params_default", "frame_sets", "build_mask", "build_mask_device",
+    "build_exact_mask_device", "attention", "attention_exact",
     "dense_attention", "WINDOW_BASIC", "WINDOW_ADAPTIVE", "WINDOW_EXPANDED",
     "MAX_FRAMES",
 ]
@@ -60,6 +64,12 @@ class BlockMask(ctypes.Structure):
                 ("row_ptr", _p), ("col_idx", _p)]
 
 
+class ExactMask(ctypes.Structure):
+    """lvsa_exact_mask: device-resident token-exact form (row_ptr + entry words)."""
+    _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_blocks", _i32),
+                ("frame_tokens", _i32), ("row_ptr", _p), ("entry", _p)]
+
+
 class _Tensor(ctypes.Structure):
     _fields_ = [("data", _p), ("heads", _i32), ("n_tokens", _i32),
                 ("head_dim", _i32), ("stride_head", _i64),
@@ -95,6 +105,18 @@ def lib():
             "lvsa_build_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                               ctypes.POINTER(Params), _p, _p,
                                               _i64, _p]),
+            "lvsa_build_exact_mask": (_i32, [_i32, _i32, _i32, _i32, _i32,
+                                             ctypes.POINTER(Params),
+                                             ctypes.POINTER(_p)]),
+            "lvsa_csr_entries": (_i32, [_p, _pi32,
+                                        ctypes.POINTER(ctypes.POINTER(ctypes.c_uint32))]),
+            "lvsa_csr_exact_view": (_i32, [_p, ctypes.POINTER(ExactMask)]),
+            "lvsa_build_exact_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
+                                                    ctypes.POINTER(Params), _p, _p,
+                                                    _i64, _p]),
+            "lvsa_attention_exact": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
+                                     [ctypes.POINTER(ExactMask),
+                                      ctypes.POINTER(_Tensor), _p]),
             "lvsa_attention": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
                                [ctypes.POINTER(BlockMask), ctypes.POINTER(_Tensor), _p]),
             "lvsa_dense_attention": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
@@ -187,6 +209,18 @@ class Csr:
                    else np.zeros(0, dtype=np.int32))
         return row_ptr, col_idx
 
+    def entries(self):
+        """Token-exact entry words as a numpy uint32 copy (raises LvsaError
+        with EUNSUPPORTED for a handle built without them)."""
+        import numpy as np
+        nnz = self.nnz
+        P = _i32()
+        e = ctypes.POINTER(ctypes.c_uint32)()
+        _check(lib().lvsa_csr_entries(self._h, ctypes.byref(P), ctypes.byref(e)),
+               "lvsa_csr_entries")
+        return (np.ctypeslib.as_array(e, shape=(nnz,)).copy() if nnz
+                else np.zeros(0, dtype=np.uint32))
+
     def upload(self, stream=None):
         _check(lib().lvsa_csr_upload(self._h, _stream_ptr(stream)), "lvsa_csr_upload")
         return self
@@ -197,13 +231,21 @@ class Csr:
                "lvsa_csr_device_view")
         return m
 
+    def exact_mask(self):
+        m = ExactMask()
+        _check(lib().lvsa_csr_exact_view(self._h, ctypes.byref(m)),
+               "lvsa_csr_exact_view")
+        return m
 
-def build_mask(T, P, B, step, params=None, layer=0):
-    """Host LVSA mask builder -> Csr."""
+
+def build_mask(T, P, B, step, params=None, layer=0, exact=False):
+    """Host LVSA mask builder -> Csr.  ``exact=True`` also builds the
+    token-exact entry words (lvsa_build_exact_mask)."""
     params = params or Params()
     h = _p()
-    _check(lib().lvsa_build_mask(T, P, B, step, layer, ctypes.byref(params),
-                                 ctypes.byref(h)), "lvsa_build_mask")
+    fn, name = ((lib().lvsa_build_exact_mask, "lvsa_build_exact_mask") if exact
+                else (lib().lvsa_build_mask, "lvsa_build_mask"))
+    _check(fn(T, P, B, step, layer, ctypes.byref(params), ctypes.byref(h)), name)
     return Csr(h.value)
 
 
@@ -222,6 +264,19 @@ def build_mask_device(T, P, B, step, row_ptr, col_idx, params=None, layer=0,
                                         col_idx.numel(), _stream_ptr(stream)),
            "lvsa_build_mask_device")
     return device_mask(T * P, B, row_ptr, col_idx)
+
+
+def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
+                            stream=None):
+    """Device builder of the token-exact form into device tensors (row_ptr
+    int32 [nb+1], entry int32/uint32 [>= nb*nb]); returns an ExactMask."""
+    params = params or Params()
+    _check(lib().lvsa_build_exact_mask_device(
+        T, P, B, step, layer, ctypes.byref(params), _p(row_ptr.data_ptr()),
+        _p(entry.data_ptr()), entry.numel(), _stream_ptr(stream)),
+        "lvsa_build_exact_mask_device")
+    nb = (T * P + B - 1) // B
+    return ExactMask(T * P, B, nb, P, row_ptr.data_ptr(), entry.data_ptr())
 
 
 def _tensor(t):
@@ -245,6 +300,19 @@ def attention(q, k, v, mask, out=None, stream=None):
     _check(lib().lvsa_attention(ctypes.byref(tq), ctypes.byref(tk), ctypes.byref(tv),
                                 ctypes.byref(mask), ctypes.byref(to),
                                 _stream_ptr(stream)), "lvsa_attention")
+    return out
+
+
+def attention_exact(q, k, v, mask, out=None, stream=None):
+    """Token-exact attention (lvsa_attention_exact): Eq. 2 token for token."""
+    import torch
+    if out is None:
+        out = torch.empty_like(q)
+    tq, tk, tv, to = (_tensor(x) for x in (q, k, v, out))
+    _check(lib().lvsa_attention_exact(ctypes.byref(tq), ctypes.byref(tk),
+                                      ctypes.byref(tv), ctypes.byref(mask),
+                                      ctypes.byref(to), _stream_ptr(stream)),
+           "lvsa_attention_exact")
     return out
 
 

@@ -52,11 +52,16 @@ struct lvsa_csr {
   int32_t n_tokens = 0;
   int32_t block = 0;
   int32_t n_blocks = 0;
+  int32_t frame_tokens = 0;
+  bool has_entry = false;          // token-exact entry words built
   std::vector<int32_t> row_ptr;
   std::vector<int32_t> col_idx;
+  std::vector<uint32_t> entry;
   int32_t* d_row_ptr = nullptr;
   int32_t* d_col_idx = nullptr;
+  uint32_t* d_entry = nullptr;
   int64_t d_col_cap = 0;
+  int64_t d_entry_cap = 0;
 };
 
 using namespace lvsa;
@@ -74,7 +79,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 100; }
+int32_t lvsa_version(void) { return 10100; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
@@ -110,9 +115,11 @@ lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
   return LVSA_OK;
 }
 
-lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
-                            int32_t layer, const lvsa_params* p,
-                            lvsa_csr** out) {
+namespace {
+
+lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
+                              int32_t layer, const lvsa_params* p,
+                              bool exact, lvsa_csr** out) {
   if (!out) return LVSA_EINVAL;
   *out = nullptr;
   if (layer < 0) return LVSA_EINVAL;
@@ -121,19 +128,38 @@ lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
   FrameCfg c;
   st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
+  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  if (exact && !exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
   lvsa_csr* h = new (std::nothrow) lvsa_csr();
   if (!h) return LVSA_ENOMEM;
+  h->has_entry = exact;
   try {
-    build_csr_host(c, P, B, &h->row_ptr, &h->col_idx);
+    build_csr_host(c, P, B, &h->row_ptr, &h->col_idx,
+                   h->has_entry ? &h->entry : nullptr);
   } catch (const std::bad_alloc&) {
     delete h;
     return LVSA_ENOMEM;
   }
   h->n_tokens = T * P;
+  h->frame_tokens = P;
   h->block = B;
   h->n_blocks = (int32_t)h->row_ptr.size() - 1;
   *out = h;
   return LVSA_OK;
+}
+
+}  // namespace
+
+lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
+                            int32_t layer, const lvsa_params* p,
+                            lvsa_csr** out) {
+  return build_mask_handle(T, P, B, step, layer, p, false, out);
+}
+
+lvsa_status lvsa_build_exact_mask(int32_t T, int32_t P, int32_t B,
+                                  int32_t step, int32_t layer,
+                                  const lvsa_params* p, lvsa_csr** out) {
+  return build_mask_handle(T, P, B, step, layer, p, true, out);
 }
 
 lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
@@ -170,6 +196,17 @@ lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
     }
     csr->d_col_cap = cap;
   }
+  if (csr->has_entry && (!csr->d_entry || csr->d_entry_cap < nnz)) {
+    if (csr->d_entry) (void)hipFree(csr->d_entry);
+    csr->d_entry = nullptr;
+    csr->d_entry_cap = 0;
+    const int64_t cap = nnz > 0 ? nnz : 1;
+    if (hipMalloc(&csr->d_entry, sizeof(uint32_t) * cap) != hipSuccess) {
+      csr->d_entry = nullptr;
+      return LVSA_ENOMEM;
+    }
+    csr->d_entry_cap = cap;
+  }
   hipStream_t s = (hipStream_t)stream;
   if (hipMemcpyAsync(csr->d_row_ptr, csr->row_ptr.data(),
                      sizeof(int32_t) * csr->row_ptr.size(),
@@ -179,15 +216,20 @@ lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
       hipMemcpyAsync(csr->d_col_idx, csr->col_idx.data(), sizeof(int32_t) * nnz,
                      hipMemcpyHostToDevice, s) != hipSuccess)
     return LVSA_EDEVICE;
+  if (csr->has_entry && nnz > 0 &&
+      hipMemcpyAsync(csr->d_entry, csr->entry.data(), sizeof(uint32_t) * nnz,
+                     hipMemcpyHostToDevice, s) != hipSuccess)
+    return LVSA_EDEVICE;
   return LVSA_OK;
 }
 
 void lvsa_csr_free(lvsa_csr* csr) {
   if (!csr) return;
-  if (csr->d_row_ptr || csr->d_col_idx) {
+  if (csr->d_row_ptr || csr->d_col_idx || csr->d_entry) {
     (void)hipDeviceSynchronize();
     if (csr->d_row_ptr) (void)hipFree(csr->d_row_ptr);
     if (csr->d_col_idx) (void)hipFree(csr->d_col_idx);
+    if (csr->d_entry) (void)hipFree(csr->d_entry);
   }
   delete csr;
 }
@@ -199,6 +241,48 @@ lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out) {
   out->n_blocks = csr->n_blocks;
   out->row_ptr = csr->d_row_ptr;
   out->col_idx = csr->d_col_idx;
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
+                             const uint32_t** entry) {
+  if (!csr) return LVSA_EINVAL;
+  if (!csr->has_entry) return LVSA_EUNSUPPORTED;
+  if (frame_tokens) *frame_tokens = csr->frame_tokens;
+  if (entry) *entry = csr->entry.data();
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out) {
+  if (!csr || !out) return LVSA_EINVAL;
+  if (!csr->has_entry) return LVSA_EUNSUPPORTED;
+  if (!csr->d_row_ptr || !csr->d_entry) return LVSA_EINVAL;
+  out->n_tokens = csr->n_tokens;
+  out->block = csr->block;
+  out->n_blocks = csr->n_blocks;
+  out->frame_tokens = csr->frame_tokens;
+  out->row_ptr = csr->d_row_ptr;
+  out->entry = csr->d_entry;
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
+                                         int32_t step, int32_t layer,
+                                         const lvsa_params* p,
+                                         int32_t* d_row_ptr, uint32_t* d_entry,
+                                         int64_t entry_capacity, void* stream) {
+  if (layer < 0 || !d_row_ptr || !d_entry) return LVSA_EINVAL;
+  lvsa_status st = check_mask_shape(T, P, B);
+  if (st != LVSA_OK) return st;
+  FrameCfg c;
+  st = resolve_frames(T, step, p, &c);
+  if (st != LVSA_OK) return st;
+  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  if (!exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
+  if (entry_capacity < nb * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry,
+                               (hipStream_t)stream) != hipSuccess)
+    return LVSA_EDEVICE;
   return LVSA_OK;
 }
 
@@ -215,7 +299,7 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
   if (st != LVSA_OK) return st;
   const int64_t nb = ((int64_t)T * P + B - 1) / B;
   if (col_capacity < nb * nb) return LVSA_EINVAL;
-  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx,
+  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr,
                                (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
@@ -237,7 +321,8 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                           const lvsa_tensor* v, int32_t n_tokens,
                           int32_t block, int32_t n_blocks,
                           const int32_t* row_ptr, const int32_t* col_idx,
-                          bool sparse, lvsa_tensor* out, void* stream) {
+                          int32_t frame_tokens, AttnMode mode,
+                          lvsa_tensor* out, void* stream) {
   if (!q || !k || !v || !out) return LVSA_EINVAL;
   if (block != 64 && block != 128) return LVSA_EUNSUPPORTED;
   const int32_t H = q->heads;
@@ -276,7 +361,8 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   a.n_blocks = n_blocks;
   a.row_ptr = row_ptr;
   a.col_idx = col_idx;
-  if (launch_attention(a, block, sparse, (hipStream_t)stream) != hipSuccess)
+  a.frame_tokens = frame_tokens;
+  if (launch_attention(a, block, mode, (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -288,7 +374,21 @@ lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            lvsa_tensor* out, void* stream) {
   if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
   return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
-                       mask->row_ptr, mask->col_idx, true, out, stream);
+                       mask->row_ptr, mask->col_idx, 0, ATTN_BLOCK, out, stream);
+}
+
+lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
+                                 const lvsa_tensor* v,
+                                 const lvsa_exact_mask* mask, lvsa_tensor* out,
+                                 void* stream) {
+  if (!mask || !mask->row_ptr || !mask->entry) return LVSA_EINVAL;
+  if (mask->frame_tokens < 1 || mask->n_tokens % mask->frame_tokens != 0)
+    return LVSA_EINVAL;
+  if (!exact_supported(mask->frame_tokens, mask->block, mask->n_blocks))
+    return LVSA_EUNSUPPORTED;
+  return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
+                       mask->row_ptr, (const int32_t*)mask->entry,
+                       mask->frame_tokens, ATTN_EXACT, out, stream);
 }
 
 lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
@@ -299,8 +399,8 @@ lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   const int32_t n = q->n_tokens;
   if (n < 1) return LVSA_EINVAL;
   const int32_t nb = (int32_t)(((int64_t)n + block - 1) / block);
-  return run_attention(q, k, v, n, block, nb, nullptr, nullptr, false, out,
-                       stream);
+  return run_attention(q, k, v, n, block, nb, nullptr, nullptr, 0, ATTN_DENSE,
+                       out, stream);
 }
 
 }  // extern "C"

@@ -307,6 +307,39 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int kh, int lane,
   }
 }
 
+// Token-exact form: the block's entry word w says which query-frame /
+// key-frame parts are attended (pattern bit 2a+b, a = the lane's query row
+// lies in the query block's second frame, b = the key lies in the key
+// block's second frame, which starts kfirst keys in).  A row's kept keys are
+// then one range [klo, khi) of the block, also clipped at `valid` = N minus
+// the block's first key.  Scores outside it become -inf.  Blocks whose every
+// part is attended and that are not ragged skip the masking.
+template <int BLOCK>
+__device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int kh, int lane,
+                                           uint32_t w, int valid,
+                                           const bool (&second)[QT]) {
+  using TL = Tile<BLOCK>;
+  const int hl = lane / 32;
+  const uint32_t pat = w >> 24;
+  if (pat != 0xFu || valid < BLOCK) {
+    const int kfirst = (int)((w >> 16) & 0xFFu);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const uint32_t bits = second[qt] ? pat >> 2 : pat;
+      const int klo = (bits & 1u) ? 0 : kfirst;
+      const int khi = (bits & 2u) ? valid : min(kfirst, valid);
+      const uint32_t width = (uint32_t)max(khi - klo, 0);
+#pragma unroll
+      for (int kt = 0; kt < TL::KTW; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = TL::KH * kh + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
+          if ((uint32_t)(key - klo) >= width) sc.s[qt][kt][r] = -__builtin_inff();
+        }
+    }
+  }
+}
+
 template <int BLOCK>
 struct Probs {
   bf16x8 p[QT][Tile<BLOCK>::KTW][2];   // [q tile][key tile][k-step half]
@@ -473,15 +506,19 @@ __device__ __forceinline__ void scores_with_softmax(
   pr.raise = any_raise;
 }
 
-template <int BLOCK, bool SPARSE>
+// MODE: ATTN_DENSE (every key block), ATTN_BLOCK (kept blocks of a block
+// CSR), ATTN_EXACT (kept blocks, col_idx holding token-exact entry words).
+template <int BLOCK, int MODE>
 __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
     const __bf16* __restrict__ vg, __bf16* __restrict__ og, int64_t q_sh,
     int64_t q_st, int64_t k_sh, int64_t k_st, int64_t v_sh, int64_t v_st,
     int64_t o_sh, int64_t o_st, int32_t H, int32_t N, int32_t nb,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
-    float scale_log2) {
+    int32_t P, float scale_log2) {
   using TL = Tile<BLOCK>;
+  constexpr bool SPARSE = MODE != ATTN_DENSE;
+  constexpr bool EXACT = MODE == ATTN_EXACT;
   // Stages: K slots 0-1, V slots 0-2.
   __shared__ __attribute__((aligned(1024))) char lds[5 * TL::BYTES];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
@@ -506,8 +543,14 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const uint32_t v_bytes = (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2);
   const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
   const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
-  auto rk_at = [&](int kb) { return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, kb, nb); };
-  auto rv_at = [&](int kb) { return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, kb, nb); };
+  // Key-block values below are block indices, or entry words in exact mode.
+  auto kb_of = [&](int w) { return EXACT ? (int)((uint32_t)w & 0xFFFFu) : w; };
+  auto rk_at = [&](int w) {
+    return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, kb_of(w), nb);
+  };
+  auto rv_at = [&](int w) {
+    return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, kb_of(w), nb);
+  };
   const FragAddr fa = frag_addr<BLOCK>(kh, lane);
 
   // Q fragments: rows qrow0 + 32*qt, k-slots d = 16*stp + 8*hl + 0..7.
@@ -522,6 +565,24 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
                         ? *(const bf16x8*)(qh + (int64_t)qrow * q_st + 16 * stp + 8 * hl)
                         : bf16x8{};
   }
+
+  // Exact mode: whether each of the lane's query rows lies in the query
+  // block's second frame (the first frame holds the block's first qfirst
+  // rows; P >= BLOCK, so there are at most two).
+  bool second[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) second[qt] = false;
+  if constexpr (EXACT) {
+    const int qfirst = P - (int)(((int64_t)qb * BLOCK) % P);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) second[qt] = qrow0 + 32 * qt - qb * BLOCK >= qfirst;
+  }
+  auto mask_block = [&](Scores<BLOCK>& sc, int w) {
+    if constexpr (EXACT)
+      mask_exact<BLOCK>(sc, kh, lane, (uint32_t)w, N - kb_of(w) * BLOCK, second);
+    else
+      mask_tail<BLOCK>(sc, kh, lane, N - w * BLOCK);
+  };
 
   int beg = 0, n = nb;
   if constexpr (SPARSE) {
@@ -565,7 +626,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     if (n > 1) issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(kb1), kp);
     Scores<BLOCK> sa, sb;
     compute_scores<BLOCK>(k_lds, qf, sa, fa);
-    mask_tail<BLOCK>(sa, kh, lane, N - kb0 * BLOCK);
+    mask_block(sa, kb0);
     wait_loads_and_sync();
 
     Probs<BLOCK> pr;
@@ -584,7 +645,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       scores_with_softmax<BLOCK>(k_lds + kslot * TL::BYTES, qf, nxt, cur, ws, pr,
                                  fa, scale_log2, sl);
       accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
-      mask_tail<BLOCK>(nxt, kh, lane, N - kb1 * BLOCK);
+      mask_block(nxt, kb1);
       kslot = 1 - kslot;
       vslot = vnext;
       wait_loads_and_sync();
@@ -655,26 +716,31 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   }
 }
 
-template <int BLOCK, bool SPARSE>
+template <int BLOCK, int MODE>
 hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)D);
   const int grid = a.n_blocks * a.heads;
-  hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, SPARSE>), dim3(grid),
+  hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, MODE>), dim3(grid),
                      dim3(Tile<BLOCK>::NT), 0, stream, (const __bf16*)a.q,
                      (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
                      a.q_sh, a.q_st, a.k_sh, a.k_st, a.v_sh, a.v_st, a.o_sh,
                      a.o_st, a.heads, a.n_tokens, a.n_blocks, a.row_ptr,
-                     a.col_idx, scale_log2);
+                     a.col_idx, a.frame_tokens, scale_log2);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int32_t block, bool sparse,
+hipError_t launch_attention(const AttnArgs& a, int32_t block, AttnMode mode,
                             hipStream_t stream) {
-  if (block == 128)
-    return sparse ? launch_t<128, true>(a, stream) : launch_t<128, false>(a, stream);
-  return sparse ? launch_t<64, true>(a, stream) : launch_t<64, false>(a, stream);
+  if (block == 128) {
+    if (mode == ATTN_EXACT) return launch_t<128, ATTN_EXACT>(a, stream);
+    if (mode == ATTN_BLOCK) return launch_t<128, ATTN_BLOCK>(a, stream);
+    return launch_t<128, ATTN_DENSE>(a, stream);
+  }
+  if (mode == ATTN_EXACT) return launch_t<64, ATTN_EXACT>(a, stream);
+  if (mode == ATTN_BLOCK) return launch_t<64, ATTN_BLOCK>(a, stream);
+  return launch_t<64, ATTN_DENSE>(a, stream);
 }
 
 }  // namespace lvsa

@@ -94,4 +94,48 @@ __host__ __device__ inline void block_frame_range(int32_t b, int32_t P,
   *last = (int32_t)((end - 1) / P);
 }
 
+// Token-exact entry word of a kept block pair (lvsa.h, "token-exact form").
+// The query block touches frames f0..f1 and key block kb frames g0..g1, each
+// at most two frames apart since P >= B; kb's first kfirst tokens lie in g0.
+// attends(t, tau) is tau in A(t).
+//   bits  0..15  kb
+//   bits 16..23  kfirst (B when kb lies in one frame)
+//   bits 24..27  bit 2a+b: frame (b ? g1 : g0) is in A(a ? f1 : f0)
+template <typename Attends>
+__host__ __device__ inline uint32_t exact_word(int32_t kb, int32_t g0,
+                                               int32_t g1, uint32_t kfirst,
+                                               int32_t f0, int32_t f1,
+                                               const Attends& attends) {
+  const uint32_t pat = (attends(f0, g0) ? 1u : 0u) | (attends(f0, g1) ? 2u : 0u) |
+                       (attends(f1, g0) ? 4u : 0u) | (attends(f1, g1) ? 8u : 0u);
+  return (uint32_t)kb | (kfirst << 16) | (pat << 24);
+}
+
+// Frames g0..g1 of key block kb and its tokens in frame g0 (B if g0 == g1).
+__host__ __device__ inline void key_block_split(int32_t kb, int32_t P,
+                                                int32_t B, int32_t N,
+                                                int32_t* g0, int32_t* g1,
+                                                uint32_t* kfirst) {
+  block_frame_range(kb, P, B, N, g0, g1);
+  *kfirst = *g1 > *g0 ? (uint32_t)((int64_t)(*g0 + 1) * P - (int64_t)kb * B)
+                      : (uint32_t)B;
+}
+
+template <typename Attends>
+__host__ __device__ inline uint32_t exact_entry(int32_t kb, int32_t f0,
+                                                int32_t f1, int32_t P,
+                                                int32_t B, int32_t N,
+                                                const Attends& attends) {
+  int32_t g0, g1;
+  uint32_t kfirst;
+  key_block_split(kb, P, B, N, &g0, &g1, &kfirst);
+  return exact_word(kb, g0, g1, kfirst, f0, f1, attends);
+}
+
+// Whether a block mask of (P, B, nb) can carry exact entry words.
+__host__ __device__ inline bool exact_supported(int32_t P, int32_t B,
+                                                int64_t nb) {
+  return P >= B && B <= 255 && nb <= 65536;
+}
+
 }  // namespace lvsa

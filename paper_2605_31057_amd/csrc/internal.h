@@ -18,15 +18,19 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
 // Checks (T, P, B) of a block mask: T*P + B must fit in int32.
 lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B);
 
-// Host CSR construction (mask_host.cpp).
+// Host CSR construction (mask_host.cpp).  `entry` (may be null) receives the
+// token-exact entry word of every kept block; callers pass it only when
+// exact_supported(P, B, nb).
 void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<int32_t>* row_ptr,
-                    std::vector<int32_t>* col_idx);
+                    std::vector<int32_t>* col_idx,
+                    std::vector<uint32_t>* entry);
 
-// Device CSR construction (mask_device.hip).
+// Device CSR construction (mask_device.hip).  Writes row_ptr and, where the
+// pointer is non-null, col_idx and/or the token-exact entry words.
 hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
-                                    hipStream_t stream);
+                                    uint32_t* d_entry, hipStream_t stream);
 
 // Attention launch (attention.hip).  Pointers are bf16 tensors; strides in
 // elements.  row_ptr/col_idx are null for the dense pass.
@@ -40,9 +44,11 @@ struct AttnArgs {
   int32_t n_tokens;
   int32_t n_blocks;
   const int32_t* row_ptr;
-  const int32_t* col_idx;
+  const int32_t* col_idx;   // block indices, or entry words (ATTN_EXACT)
+  int32_t frame_tokens;     // P (ATTN_EXACT only)
 };
-hipError_t launch_attention(const AttnArgs& a, int32_t block, bool sparse,
+enum AttnMode { ATTN_DENSE = 0, ATTN_BLOCK = 1, ATTN_EXACT = 2 };
+hipError_t launch_attention(const AttnArgs& a, int32_t block, AttnMode mode,
                             hipStream_t stream);
 
 }  // namespace lvsa

@@ -10,7 +10,8 @@
 //   2. one thread per query block: count its kept key blocks into
 //      row_ptr[qb + 1];
 //   3. in-place exclusive scan of the counts (chunks of 1024, LDS tree);
-//   4. one thread per query block: write its row of col_idx.
+//   4. one thread per query block: write its row of col_idx and/or of the
+//      token-exact entry words.
 // The metadata is tiny (T <= 4096 frames), so one workgroup keeps the whole
 // build in a single launch with plain __syncthreads between phases.
 #include "internal.h"
@@ -47,7 +48,7 @@ __device__ inline void for_each_kept(const Rows& r, int32_t qb, F&& emit) {
 
 __global__ __launch_bounds__(kThreads) void build_mask_kernel(
     FrameCfg c, int32_t P, int32_t B, int32_t* __restrict__ row_ptr,
-    int32_t* __restrict__ col_idx) {
+    int32_t* __restrict__ col_idx, uint32_t* __restrict__ entry) {
   __shared__ uint8_t s_anchor[LVSA_MAX_FRAMES];
   __shared__ int16_t s_lo[LVSA_MAX_FRAMES];
   __shared__ int16_t s_hi[LVSA_MAX_FRAMES];
@@ -98,10 +99,19 @@ __global__ __launch_bounds__(kThreads) void build_mask_kernel(
     __syncthreads();
   }
 
+  auto attends = [&](int32_t t, int32_t tau) {
+    return s_anchor[tau] != 0 || (s_lo[t] <= tau && tau <= s_hi[t]);
+  };
   for (int32_t qb = tid; qb < nb; qb += kThreads) {
-    int32_t* dst = col_idx + row_ptr[qb];
+    const int32_t beg = row_ptr[qb];
+    int32_t f0, f1;
+    block_frame_range(qb, P, B, N, &f0, &f1);
     int32_t n = 0;
-    for_each_kept(r, qb, [&](int32_t b) { dst[n++] = b; });
+    for_each_kept(r, qb, [&](int32_t b) {
+      if (col_idx) col_idx[beg + n] = b;
+      if (entry) entry[beg + n] = exact_entry(b, f0, f1, P, B, N, attends);
+      ++n;
+    });
   }
 }
 
@@ -109,9 +119,9 @@ __global__ __launch_bounds__(kThreads) void build_mask_kernel(
 
 hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
-                                    hipStream_t stream) {
+                                    uint32_t* d_entry, hipStream_t stream) {
   hipLaunchKernelGGL(build_mask_kernel, dim3(1), dim3(kThreads), 0, stream, c,
-                     P, B, d_row_ptr, d_col_idx);
+                     P, B, d_row_ptr, d_col_idx, d_entry);
   return hipGetLastError();
 }
 

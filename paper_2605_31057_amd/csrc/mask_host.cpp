@@ -12,6 +12,9 @@
 // at a shared straddling block, so a running "last emitted" index keeps the
 // row ascending and free of repeats.  Consecutive query blocks that touch
 // the same frames have identical rows, which are copied.
+//
+// The token-exact entry words (lvsa.h) are built alongside when asked for:
+// one word per kept block, from the two (at most) frames of each side.
 #include <algorithm>
 #include <cstring>
 
@@ -21,7 +24,8 @@ namespace lvsa {
 
 void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<int32_t>* row_ptr,
-                    std::vector<int32_t>* col_idx) {
+                    std::vector<int32_t>* col_idx,
+                    std::vector<uint32_t>* entry) {
   const int32_t T = c.T;
   const int32_t N = T * P;
   const int32_t nb = ceil_div(N, B);
@@ -31,21 +35,35 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
     anchor[t] = is_anchor(c, t) ? 1 : 0;
     frame_window(c, t, &lo[t], &hi[t]);
   }
+  auto attends = [&](int32_t t, int32_t tau) {
+    return anchor[tau] != 0 || (lo[t] <= tau && tau <= hi[t]);
+  };
+  // Per key block: its frames and split point, so an entry word costs four
+  // table lookups.
+  std::vector<int32_t> kg0, kg1;
+  std::vector<uint32_t> kfirst;
+  if (entry) {
+    kg0.resize(nb);
+    kg1.resize(nb);
+    kfirst.resize(nb);
+    for (int32_t b = 0; b < nb; ++b)
+      key_block_split(b, P, B, N, &kg0[b], &kg1[b], &kfirst[b]);
+  }
+
+  // Pass 1: the distinct rows (one per run of query blocks touching the same
+  // frames) into small scratch arrays, and every row's length.
+  std::vector<int32_t> uniq;
+  std::vector<uint32_t> uniq_e;
+  std::vector<int64_t> src(nb);
   row_ptr->assign(nb + 1, 0);
-  col_idx->clear();
-  col_idx->reserve((size_t)nb * 64);
   std::vector<uint8_t> attended(T);
   int32_t prev_first = -1, prev_last = -1;
   int64_t prev_begin = 0, prev_len = 0;
   for (int32_t qb = 0; qb < nb; ++qb) {
     int32_t f0, f1;
     block_frame_range(qb, P, B, N, &f0, &f1);
-    const int64_t begin = (int64_t)col_idx->size();
-    if (f0 == prev_first && f1 == prev_last) {
-      col_idx->resize(begin + prev_len);
-      std::memcpy(col_idx->data() + begin, col_idx->data() + prev_begin,
-                  prev_len * sizeof(int32_t));
-    } else {
+    if (f0 != prev_first || f1 != prev_last) {
+      prev_begin = (int64_t)uniq.size();
       std::memcpy(attended.data(), anchor.data(), T);
       for (int32_t t = f0; t <= f1; ++t)
         std::fill(attended.begin() + lo[t], attended.begin() + hi[t] + 1, 1);
@@ -54,16 +72,30 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
         if (!attended[tau]) continue;
         const int32_t b0 = (int32_t)((int64_t)tau * P / B);
         const int32_t b1 = (int32_t)(((int64_t)tau * P + P - 1) / B);
-        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b)
-          col_idx->push_back(b);
+        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b) {
+          uniq.push_back(b);
+          if (entry)
+            uniq_e.push_back(exact_word(b, kg0[b], kg1[b], kfirst[b], f0, f1, attends));
+        }
         last = std::max(last, b1);
       }
+      prev_len = (int64_t)uniq.size() - prev_begin;
       prev_first = f0;
       prev_last = f1;
     }
-    prev_begin = begin;
-    prev_len = (int64_t)col_idx->size() - begin;
-    (*row_ptr)[qb + 1] = (int32_t)col_idx->size();
+    src[qb] = prev_begin;
+    (*row_ptr)[qb + 1] = (*row_ptr)[qb] + (int32_t)prev_len;
+  }
+
+  // Pass 2: one allocation of the final size, rows copied in.
+  const int64_t nnz = (*row_ptr)[nb];
+  col_idx->resize(nnz);
+  if (entry) entry->resize(nnz);
+  for (int32_t qb = 0; qb < nb; ++qb) {
+    const int64_t dst = (*row_ptr)[qb], len = (*row_ptr)[qb + 1] - dst;
+    std::memcpy(col_idx->data() + dst, uniq.data() + src[qb], len * sizeof(int32_t));
+    if (entry)
+      std::memcpy(entry->data() + dst, uniq_e.data() + src[qb], len * sizeof(uint32_t));
   }
 }
 

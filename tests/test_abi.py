@@ -204,3 +204,122 @@ def test_attention_rejects_before_launch():
         L.EUNSUPPORTED
     assert lib.lvsa_dense_attention(ref(q), ref(k), ref(_t(0x30000, heads=1)), 128,
                                     ref(o), None) == L.EINVAL
+
+
+# ------------------------------------------------------ token-exact form ---
+
+def decode_entries(row_ptr, col_idx, entry, T, P, B):
+    """Token mask described by the entry words (the token-exact form that
+    include/lvsa.h defines), checking each word's fixed fields on the way."""
+    N = T * P
+    nb = -(-N // B)
+    tm = np.zeros((N, N), dtype=bool)
+    tok_frame = np.arange(N) // P
+    for qb in range(nb):
+        rows = np.arange(qb * B, min((qb + 1) * B, N))
+        a = (tok_frame[rows] != (qb * B) // P).astype(np.int64)
+        for idx in range(row_ptr[qb], row_ptr[qb + 1]):
+            w = int(entry[idx])
+            kb = int(col_idx[idx])
+            assert w & 0xFFFF == kb and w >> 28 == 0, hex(w)
+            kfirst, pat = (w >> 16) & 0xFF, (w >> 24) & 0xF
+            cols = np.arange(kb * B, min((kb + 1) * B, N))
+            g0 = (kb * B) // P
+            b = (tok_frame[cols] != g0).astype(np.int64)
+            straddles = (min((kb + 1) * B, N) - 1) // P != g0
+            assert kfirst == ((g0 + 1) * P - kb * B if straddles else B), (qb, kb)
+            assert np.array_equal(b, (cols - kb * B >= kfirst).astype(np.int64))
+            bit = 2 * a[:, None] + b[None, :]
+            tm[np.ix_(rows, cols)] = ((pat >> bit) & 1).astype(bool)
+    return tm
+
+
+EXACT_CASES = [  # T, P, B: P >= B, mostly P mod B != 0 and a ragged last block
+    (5, 200, 128), (7, 100, 64), (6, 130, 128), (4, 128, 128), (9, 70, 64),
+    (3, 255, 128), (12, 96, 64),
+]
+
+
+@pytest.mark.parametrize("T,P,B", EXACT_CASES)
+def test_host_entries_decode_to_oracle_token_mask(T, P, B):
+    """Bit-exact: the entry words of the host builder describe exactly Eq. 2's
+    token mask from the oracle, for every window rule and several steps."""
+    for mode, rotate, tie_high in [(2, 1, 0), (2, 1, 1), (1, 1, 0), (0, 0, 0), (2, 0, 0)]:
+        for s in (0, 1, 3):
+            p = L.Params(budget_frames=0, window=1, tper=3, window_mode=mode,
+                         rotate=rotate, tie_high=tie_high)
+            csr = L.build_mask(T, P, B, s, p, exact=True)
+            blk = L.build_mask(T, P, B, s, p)
+            row_ptr, col_idx = csr.arrays()
+            assert all(np.array_equal(x, y) for x, y in zip(blk.arrays(), (row_ptr, col_idx)))
+            got = decode_entries(row_ptr, col_idx, csr.entries(), T, P, B)
+            _, _, A = M.attended_frames(T, s, W=1, tper=3, mode=mode,
+                                        rotate=bool(rotate), tie_high=bool(tie_high))
+            assert np.array_equal(got, M.token_mask(A, T, P)), (mode, rotate, s)
+
+
+def test_entries_full_when_block_divides_frame_and_unsupported_below_block():
+    p = L.Params(budget_frames=0, window=1, tper=3)
+    csr = L.build_mask(6, 256, 128, 2, p, exact=True)
+    e = csr.entries()
+    assert len(e) == csr.nnz and all(int(w) >> 24 == 0xF for w in e)
+    m = L.ExactMask()
+    assert L.lib().lvsa_csr_exact_view(csr._h, ctypes.byref(m)) == L.EINVAL  # no upload
+    # P < B: no exact form; a block-only handle carries no entry words.
+    out = ctypes.c_void_p(123)
+    assert L.lib().lvsa_build_exact_mask(6, 100, 128, 0, 0, ctypes.byref(p),
+                                         ctypes.byref(out)) == L.EUNSUPPORTED
+    assert out.value is None
+    blk = L.build_mask(6, 256, 128, 2, p)
+    with pytest.raises(L.LvsaError) as ei:
+        blk.entries()
+    assert ei.value.status == L.EUNSUPPORTED
+    assert L.lib().lvsa_csr_exact_view(blk._h, ctypes.byref(m)) == L.EUNSUPPORTED
+
+
+def test_wan_horizon_entries_decode_on_sampled_rows():
+    """Wan 6x shape (P = 1560, B = 128): the entry words of sampled query
+    blocks give each query token exactly the keys of its frame set."""
+    T, P, B, s = 121, 1560, 128, 10
+    csr = L.build_mask(T, P, B, s, L.Params(), exact=True)
+    row_ptr, col_idx = csr.arrays()
+    entry = csr.entries()
+    _, _, A = M.attended_frames(T, s, C=21, W=6)
+    N = T * P
+    for qb in (0, 12, 13, 700, 1474):
+        for i in (qb * B, min(qb * B + B, N) - 1, qb * B + 40):
+            got = np.zeros(N, dtype=bool)
+            a = int((i // P) != (qb * B) // P)
+            for idx in range(row_ptr[qb], row_ptr[qb + 1]):
+                w = int(entry[idx])
+                kb, kfirst, pat = w & 0xFFFF, (w >> 16) & 0xFF, (w >> 24) & 0xF
+                for j in range(kb * B, min((kb + 1) * B, N)):
+                    got[j] = (pat >> (2 * a + int(j - kb * B >= kfirst))) & 1
+            want = np.array([(j // P) in A[i // P] for j in range(N)])
+            assert np.array_equal(got, want), (qb, i)
+
+
+def test_exact_attention_and_builder_reject_before_launch():
+    lib = L.lib()
+    ref = ctypes.byref
+    p = L.Params()
+    fake = ctypes.c_void_p(0x1000)
+    nb = 1475
+    assert lib.lvsa_build_exact_mask_device(121, 1560, 128, 0, 0, ref(p), fake, fake,
+                                            nb * nb - 1, None) == L.EINVAL
+    assert lib.lvsa_build_exact_mask_device(121, 100, 128, 0, 0, ref(p), fake, fake,
+                                            1 << 30, None) == L.EUNSUPPORTED
+    assert lib.lvsa_build_exact_mask_device(121, 1560, 128, 0, 0, ref(p), fake, None,
+                                            nb * nb, None) == L.EINVAL
+    n = 1000
+    nbk = -(-n // 128)
+    q, k, v, o = _t(0x10000), _t(0x20000), _t(0x30000), _t(0x40000)
+    cases = [
+        (L.ExactMask(n, 128, nbk, 100, 0x2000, 0x3000), L.EUNSUPPORTED),  # P < B
+        (L.ExactMask(n, 128, nbk, 300, 0x2000, 0x3000), L.EINVAL),    # N % P != 0
+        (L.ExactMask(n, 128, nbk, 200, 0x2000, 0), L.EINVAL),         # no entries
+        (L.ExactMask(n, 96, 11, 200, 0x2000, 0x3000), L.EUNSUPPORTED),  # block
+    ]
+    for m, want in cases:
+        assert lib.lvsa_attention_exact(ref(q), ref(k), ref(v), ref(m), ref(o),
+                                        None) == want, (m.frame_tokens, m.block)
