@@ -28,6 +28,9 @@ Readings where the paper is silent (each is listed in the design notes):
     of the query block and some token of the key block belong to an attended
     frame pair (any-overlap superset of Eq. 2; equal to it when B divides P).
   * Blocks are ceil(N / B); the last one may be ragged.
+  * Dedicated initial anchors (``extra``, the generalization named after
+    Def. 2) are frames 0..extra-1 added to G; they count as global frames in
+    Alg. 1 and come out of the budget before the period is derived.
 
 Parity pins: tests/test_oracle_mask.py (hand-worked examples under
 tests/golden/, the invariants the paper states, brute force over tokens).
@@ -43,28 +46,37 @@ def ceil_div(a, b):
     return -(-a // b)
 
 
-def anchor_period(T, C, W, tper=0):
+def anchor_period(T, C, W, tper=0, extra=0):
     """T_per (Sec. 2, budget paragraph): ceil(T / (C - (2W+1))) when C > 2W+1.
 
     A positive ``tper`` is an explicit override of the derived value.
+    ``extra`` dedicated initial anchors (the generalization Sec. 2 mentions
+    after Def. 2) take their frames out of the budget first:
+    ceil(T / (C - (2W+1) - extra)), which needs C > 2W+1+extra.
     """
     if tper > 0:
         return tper
-    if C <= 2 * W + 1:
-        raise ValueError("the derived anchor period needs C > 2W+1")
-    return ceil_div(T, C - (2 * W + 1))
+    spare = C - (2 * W + 1) - extra
+    if spare <= 0:
+        raise ValueError("the derived anchor period needs C > 2W+1+extra")
+    return ceil_div(T, spare)
 
 
-def anchors(T, T_per, s, rotate=True):
+def anchors(T, T_per, s, rotate=True, extra=0):
     """Global anchor frames as a Python set.
 
     rotate=False: Def. 2's fixed set {t : t mod T_per == 0}.
     rotate=True:  Eq. 3, G^s = {(s mod T_per + i*T_per) mod T : i = 0..ceil(T/T_per)-1}.
+    extra > 0:    the first ``extra`` frames 0..extra-1 join the set as
+                  dedicated initial anchors (e.g. extra = 1 keeps frame 0, the
+                  scene-establishing frame, at every step).
     """
     if not rotate:
-        return {t for t in range(T) if t % T_per == 0}
-    k = ceil_div(T, T_per)
-    return {((s % T_per) + i * T_per) % T for i in range(k)}
+        G = {t for t in range(T) if t % T_per == 0}
+    else:
+        k = ceil_div(T, T_per)
+        G = {((s % T_per) + i * T_per) % T for i in range(k)}
+    return G | set(range(min(extra, T)))
 
 
 def basic_window(t, W, T):
@@ -121,13 +133,13 @@ def window(t, G, W, T, mode, tie_high=False):
 
 
 def attended_frames(T, s, C=21, W=6, tper=0, mode=WINDOW_EXPANDED,
-                    rotate=True, tie_high=False):
+                    rotate=True, tie_high=False, extra=0):
     """A(t) = G^s  union  window(t) for every query frame t (Def. 2, Eq. 3).
 
     Returns (T_per, G, [A(0), ..., A(T-1)]) with each A(t) a Python set.
     """
-    T_per = anchor_period(T, C, W, tper)
-    G = anchors(T, T_per, s, rotate)
+    T_per = anchor_period(T, C, W, tper, extra)
+    G = anchors(T, T_per, s, rotate, extra)
     A = []
     for t in range(T):
         l, h = window(t, G, W, T, mode, tie_high)
@@ -229,12 +241,12 @@ def to_csr(rows):
 
 
 def build_mask(T, P, B, s, C=21, W=6, tper=0, mode=WINDOW_EXPANDED,
-               rotate=True, tie_high=False, layer=0):
+               rotate=True, tie_high=False, layer=0, extra=0):
     """The whole LVSA mask for one denoising step: (row_ptr, col_idx).
 
     ``layer`` is accepted and ignored: the paper's pattern is the same for
     every layer and head.
     """
     del layer
-    _, _, A = attended_frames(T, s, C, W, tper, mode, rotate, tie_high)
+    _, _, A = attended_frames(T, s, C, W, tper, mode, rotate, tie_high, extra)
     return to_csr(block_keep_incidence(A, T, P, B))

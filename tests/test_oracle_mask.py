@@ -302,3 +302,47 @@ def test_block_rule_is_smallest_cover_of_token_mask(T, P, B):
             for kb in range(nb):
                 tile = tm[qb * B:min((qb + 1) * B, N), kb * B:min((kb + 1) * B, N)]
                 assert (kb in kept) == bool(tile.any()), (s, qb, kb)
+
+
+# ---------------------------------------------------- extra anchors ---
+
+def test_golden_extra_anchors():
+    n = 0
+    for line in _lines("extra_anchors.txt"):
+        kind, rest = line.split(None, 1)
+        if kind == "G":
+            lhs, tper_s, frames = rest.split(":")
+            T, C, W, tper, s, rotate, E = map(int, lhs.split())
+            T_per = M.anchor_period(T, C, W, tper, E)
+            assert T_per == int(tper_s), line
+            assert sorted(M.anchors(T, T_per, s, bool(rotate), E)) == \
+                list(map(int, frames.split())), line
+        else:
+            lhs, frames = rest.split(":")
+            T, C, W, tper, s, rotate, E, t = map(int, lhs.split())
+            _, _, A = M.attended_frames(T, s, C, W, tper, rotate=bool(rotate), extra=E)
+            assert sorted(A[t]) == list(map(int, frames.split())), line
+        n += 1
+    assert n >= 12
+
+
+@pytest.mark.parametrize("E", [1, 2, 3])
+def test_extra_anchors_invariants(E):
+    """Frames 0..E-1 are in every A(t); the Alg. 1 identity |A(t)| = |G| +
+    min(2W+1, T-|G|) still holds; E = 0 is the plain rule; with the derived
+    period the budget C is never exceeded once T >= C."""
+    for T in (9, 21, 40, 121):
+        for W in (0, 1, 3, 6):
+            C = 2 * W + 1 + E + 3
+            for s in range(0, 20, 3):
+                for rotate in (True, False):
+                    T_per, G, A = M.attended_frames(T, s, C, W, rotate=rotate, extra=E)
+                    _, G0, _ = M.attended_frames(T, s, C, W, tper=T_per, rotate=rotate)
+                    assert G == G0 | set(range(min(E, T)))
+                    for t in range(T):
+                        assert set(range(min(E, T))) <= A[t]
+                        assert len(A[t]) == len(G) + min(2 * W + 1, T - len(G))
+                        if T >= C:
+                            assert len(A[t]) <= C
+    with pytest.raises(ValueError):
+        M.anchor_period(21, 14, 6, extra=1)   # C - (2W+1) - E = 0
