@@ -10,8 +10,10 @@ rotate as in a denoising loop.  Inputs are resident in HBM before timing.
 
 Prints ONE JSON line.  Besides the step throughput it reports the attention
 call alone (hipEvents), the token-exact form of the same mask (Eq. 2 token
-for token), the dense kernel of the same design, the roofline position of the
-sparse kernel, and the CPU oracle on a bounded sample.
+for token), the pattern variants of Sec. 2 (window rule, fixed vs rotating
+anchors, a dedicated initial anchor: density and call time), the dense kernel
+of the same design, the roofline position of the sparse kernel, and the CPU
+oracle on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload wan13_6x]
 """
@@ -133,6 +135,7 @@ def main():
     ap.add_argument("--workload", default="wan13_6x")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-patterns", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--pmc", action="store_true",
                     help="counter-collection run: a few untimed sparse, dense and "
@@ -261,6 +264,38 @@ def main():
         m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
                                 params=params, stream=stream)
 
+    # Pattern variants of Sec. 2 at the same step: window rule, fixed vs
+    # rotating anchors, a dedicated initial anchor.  Block density, token
+    # density (Eq. 2) and the block-sparse call time of each.
+    variants = []
+    if not args.no_patterns:
+        print("[bench] pattern variants", file=sys.stderr, flush=True)
+        names = {L.WINDOW_BASIC: "basic", L.WINDOW_ADAPTIVE: "adaptive",
+                 L.WINDOW_EXPANDED: "expanded"}
+        for mode, rotate, extra in [(L.WINDOW_EXPANDED, 1, 0), (L.WINDOW_ADAPTIVE, 1, 0),
+                                    (L.WINDOW_BASIC, 1, 0), (L.WINDOW_EXPANDED, 0, 0),
+                                    (L.WINDOW_EXPANDED, 1, 1)]:
+            pv = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
+                          window_mode=mode, rotate=rotate, extra_anchors=extra)
+            csr = L.build_mask(w.frames, w.tokens_per_frame, w.block, s_ref, pv)
+            hrp, hci = csr.arrays()
+            csr.upload(stream)
+            mv = csr.device_mask()
+            v_ms = median(time_calls(
+                lambda: L.attention(q, k, v, mv, out=out, stream=stream), 10, 2))
+            fl = kept_flops(hrp, hci, w.n_tokens, w.block, w.heads)
+            tper, anc, lo, hi = L.frame_sets(w.frames, s_ref, pv)
+            sizes = [len(set(anc) | set(range(lo[t], hi[t] + 1))) for t in range(w.frames)]
+            variants.append({
+                "window": names[mode], "rotate": bool(rotate), "extra_anchors": extra,
+                "T_per": tper, "frames_per_query_min": min(sizes),
+                "frames_per_query_max": max(sizes),
+                "block_density": int(hrp[-1]) / (nb * nb),
+                "token_density": sum(sizes) / w.frames ** 2,
+                "ms_per_call": v_ms, "tflops_kept": fl / (v_ms * 1e-3) / 1e12,
+            })
+            csr.free()
+
     dense = {}
     if not args.no_dense:
         print("[bench] dense", file=sys.stderr, flush=True)
@@ -306,6 +341,7 @@ def main():
         "nnz_step10": nnz_of[s_ref],
         "block_density_step10": nnz_of[s_ref] / (nb * nb),
         **exact,
+        **({"pattern_variants": variants} if variants else {}),
         **dense,
         "roofline": {
             "kernel": "attn_fwd_kernel<128, sparse>",

@@ -77,9 +77,18 @@ typedef struct lvsa_params {
                             0: Def. 2's fixed G = {t : t mod T_per = 0}.     */
   int32_t tie_high;      /* Alg. 1 leaves equal room unresolved: 0 extends the
                             low side (default), 1 the high side.            */
+  int32_t extra_anchors; /* E >= 0 dedicated initial anchors (the
+                            generalization named after Def. 2): frames
+                            0..E-1 join G at every step, count as global
+                            frames in Alg. 1, and leave the budget before
+                            the period is derived, T_per = ceil(T / (C -
+                            (2W+1) - E)) (needs C > 2W+1+E when tper == 0).
+                            E = 1 keeps frame 0 an anchor at every step.
+                            Default 0.                                      */
 } lvsa_params;
 
-/* Fills *p with C = 21, W = 6, tper = 0, EXPANDED, rotate = 1, tie_high = 0.
+/* Fills *p with C = 21, W = 6, tper = 0, EXPANDED, rotate = 1, tie_high = 0,
+ * extra_anchors = 0.
  * C = 21 is the paper's Wan 2.1 budget ((81-1)/4 + 1 frames); the paper does
  * not print W, and 6 is the smallest W that keeps |A(t)| within two frames of
  * C and Alg. 1 within eight iterations on every Wan horizon. */
@@ -92,10 +101,11 @@ void lvsa_params_default(lvsa_params* p);
  * Outputs (host memory, caller-owned; any may be NULL to skip it):
  *   tper_out      the anchor period T_per used
  *   anchors       [T] ascending anchor frames; *n_anchors = |G^s| = ceil(T/T_per)
+ *                 plus the extra anchors 0..E-1 that Eq. 3 did not place
  *   win_lo/win_hi [T] window bounds per query frame, so that
  *                 A(t) = anchors  U  [win_lo[t], win_hi[t]]
- * Errors: EINVAL for T, step or params out of range (including C <= 2W+1
- * with tper == 0, and a null params pointer). */
+ * Errors: EINVAL for T, step or params out of range (including C <= 2W+1+E
+ * with tper == 0, E < 0, and a null params pointer). */
 #define LVSA_MAX_FRAMES 4096
 lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
                             int32_t* tper_out, int32_t* anchors,

@@ -47,13 +47,16 @@ class LvsaError(RuntimeError):
 
 
 class Params(ctypes.Structure):
-    """lvsa_params: C, W, T_per override, window rule, rotation, tie rule."""
+    """lvsa_params: C, W, T_per override, window rule, rotation, tie rule,
+    dedicated initial anchors."""
     _fields_ = [("budget_frames", _i32), ("window", _i32), ("tper", _i32),
-                ("window_mode", _i32), ("rotate", _i32), ("tie_high", _i32)]
+                ("window_mode", _i32), ("rotate", _i32), ("tie_high", _i32),
+                ("extra_anchors", _i32)]
 
     def __init__(self, **kw):
         d = dict(budget_frames=21, window=6, tper=0,
-                 window_mode=WINDOW_EXPANDED, rotate=1, tie_high=0)
+                 window_mode=WINDOW_EXPANDED, rotate=1, tie_high=0,
+                 extra_anchors=0)
         d.update(kw)
         super().__init__(**{k: int(v) for k, v in d.items()})
 

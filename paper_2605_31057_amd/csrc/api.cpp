@@ -17,12 +17,15 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
   if ((p->rotate != 0 && p->rotate != 1) || (p->tie_high != 0 && p->tie_high != 1))
     return LVSA_EINVAL;
   if (p->tper < 0) return LVSA_EINVAL;
+  if (p->extra_anchors < 0 || p->extra_anchors > LVSA_MAX_FRAMES) return LVSA_EINVAL;
   int32_t tper = p->tper;
   if (tper == 0) {
-    // Sec. 2, budget paragraph: T_per = ceil(T / (C - (2W+1))), for C > 2W+1.
-    const int32_t spare = p->budget_frames - (2 * p->window + 1);
+    // Sec. 2, budget paragraph: T_per = ceil(T / (C - (2W+1))), for C > 2W+1;
+    // dedicated initial anchors leave the budget first.
+    const int64_t spare = (int64_t)p->budget_frames - (2 * (int64_t)p->window + 1) -
+                          p->extra_anchors;
     if (p->budget_frames <= 0 || spare <= 0) return LVSA_EINVAL;
-    tper = ceil_div(T, spare);
+    tper = ceil_div(T, (int32_t)spare);
   }
   FrameCfg c;
   c.T = T;
@@ -33,6 +36,9 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
   c.mode = p->window_mode;
   c.rotate = p->rotate;
   c.tie_high = p->tie_high;
+  c.extra = p->extra_anchors;
+  c.g = 0;
+  for (int32_t f = 0; f < T; ++f) c.g += is_anchor(c, f) ? 1 : 0;
   *out = c;
   return LVSA_OK;
 }
@@ -79,7 +85,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 10100; }
+int32_t lvsa_version(void) { return 10200; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
@@ -89,6 +95,7 @@ void lvsa_params_default(lvsa_params* p) {
   p->window_mode = LVSA_WINDOW_EXPANDED;
   p->rotate = 1;
   p->tie_high = 0;
+  p->extra_anchors = 0;
 }
 
 lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,

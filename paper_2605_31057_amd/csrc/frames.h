@@ -16,7 +16,9 @@ struct FrameCfg {
   int32_t T;         // frames
   int32_t W;         // window half-width
   int32_t tper;      // anchor period T_per
-  int32_t k;         // |G^s| = ceil(T / T_per)
+  int32_t k;         // Eq. 3 anchors ceil(T / T_per)
+  int32_t extra;     // dedicated initial anchors: frames 0..extra-1
+  int32_t g;         // |G|: Eq. 3 (or Def. 2) anchors plus the extra ones
   int32_t s0;        // s mod T_per (0 for fixed anchors)
   int32_t mode;      // LVSA_WINDOW_*
   int32_t rotate;    // Eq. 3 (1) or Def. 2's fixed set (0)
@@ -34,7 +36,9 @@ __host__ __device__ inline int32_t imax(int32_t a, int32_t b) { return a > b ? a
 //   rotate = 1: Eq. 3, f = (s0 + i*T_per) mod T for some 0 <= i < k.  The
 //   unreduced value s0 + i*T_per is below k*T_per <= T + T_per - 1 < 2T, so
 //   it equals either f or f + T.
+//   f < extra: a dedicated initial anchor.
 __host__ __device__ inline bool is_anchor(const FrameCfg& c, int32_t f) {
+  if (f < c.extra) return true;
   if (!c.rotate) return f % c.tper == 0;
   if (f >= c.s0 && (f - c.s0) % c.tper == 0 && (f - c.s0) / c.tper < c.k)
     return true;
@@ -64,7 +68,7 @@ __host__ __device__ inline int32_t frame_window(const FrameCfg& c, int32_t t,
   hi = imin(T - 1, imax(t + W, 2 * W));
   int32_t steps = 0;
   if (c.mode == LVSA_WINDOW_EXPANDED) {
-    const int32_t target = imin(2 * W + 1, T - c.k);
+    const int32_t target = imin(2 * W + 1, T - c.g);
     int32_t nonglobal = 0;
     for (int32_t f = lo; f <= hi; ++f) nonglobal += is_anchor(c, f) ? 0 : 1;
     while (nonglobal < target && (lo > 0 || hi < T - 1)) {

@@ -41,13 +41,13 @@ def test_status_strings_and_version():
         assert lib.lvsa_status_str(s)
     assert lib.lvsa_version() >= 100
     p = L.params_default()
-    assert (p.budget_frames, p.window, p.tper, p.window_mode, p.rotate, p.tie_high) == \
-        (21, 6, 0, L.WINDOW_EXPANDED, 1, 0)
+    assert (p.budget_frames, p.window, p.tper, p.window_mode, p.rotate, p.tie_high,
+            p.extra_anchors) == (21, 6, 0, L.WINDOW_EXPANDED, 1, 0, 0)
 
 
 def _oracle_kw(p):
     return dict(C=p.budget_frames, W=p.window, tper=p.tper, mode=p.window_mode,
-                rotate=bool(p.rotate), tie_high=bool(p.tie_high))
+                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors)
 
 
 def _check_frames(T, s, p):
@@ -90,7 +90,7 @@ def test_host_builder_matches_oracle_rules(mode, rotate, tie_high):
         W = rng.randint(0, 6)
         tper = rng.randint(1, T)
         p = L.Params(window=W, tper=tper, window_mode=mode, rotate=rotate,
-                     tie_high=tie_high)
+                     tie_high=tie_high, extra_anchors=rng.choice([0, 0, 1, 2, 5]))
         s = rng.randint(0, 3 * tper)
         _check_frames(T, s, p)
         P = rng.randint(1, 40)
@@ -103,6 +103,23 @@ def test_host_builder_derived_period_and_wan_horizons():
         p = L.Params()
         for s in (0, 5, 13):
             _check_csr(T, 1560, 128, s, p)
+
+
+@pytest.mark.parametrize("E", [1, 2])
+def test_host_builder_extra_anchors_derived_period(E):
+    """Dedicated initial anchors with the budget-derived period on the Wan
+    and HV horizons (C = 21 and 33, W = 6), against the oracle."""
+    for T, C, P in ((21, 21, 1560), (121, 21, 1560), (65, 33, 1590)):
+        p = L.Params(budget_frames=C, window=6, extra_anchors=E)
+        for s in (0, 7, 10, 17):
+            _check_frames(T, s, p)
+            _check_csr(T, P, 128, s, p)
+    ref = ctypes.byref
+    out = ctypes.c_void_p()
+    bad = L.Params(budget_frames=14, window=6, extra_anchors=1)   # C = 2W+1+E
+    assert L.lib().lvsa_build_mask(121, 1560, 128, 0, 0, ref(bad), ref(out)) == L.EINVAL
+    neg = L.Params(extra_anchors=-1)
+    assert L.lib().lvsa_build_mask(121, 1560, 128, 0, 0, ref(neg), ref(out)) == L.EINVAL
 
 
 def test_host_builder_layer_independent():

@@ -6,9 +6,13 @@ import sys
 import pytest
 import torch
 
+import numpy as np
+
 import paper_2605_31057_amd as L
 from paper_2605_31057_amd.inputs import WORKLOADS, make_qkv
+from oracle import attention as OA
 from oracle import mask as M
+from tests.gpu_util import assert_close
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +37,7 @@ def _device_csr(T, P, B, step, p, layer=0):
 
 def _kw(p):
     return dict(C=p.budget_frames, W=p.window, tper=p.tper, mode=p.window_mode,
-                rotate=bool(p.rotate), tie_high=bool(p.tie_high))
+                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors)
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
@@ -60,7 +64,8 @@ def test_device_builder_matches_oracle_random(mode):
     for _ in range(40):
         T = rng.randint(1, 60)
         p = L.Params(window=rng.randint(0, 6), tper=rng.randint(1, T), window_mode=mode,
-                     rotate=rng.randint(0, 1), tie_high=rng.randint(0, 1))
+                     rotate=rng.randint(0, 1), tie_high=rng.randint(0, 1),
+                     extra_anchors=rng.choice([0, 0, 1, 3]))
         P = rng.randint(1, 300)
         B = rng.choice([1, 3, 16, 64, 128])
         if -(-(T * P) // B) > 1500:
@@ -87,3 +92,44 @@ def test_device_mask_attention_equals_host_mask_attention():
         b = L.attention(q, k, v, m)
         torch.cuda.synchronize()
         assert torch.equal(a, b)
+
+
+# Window rule, anchor rotation and dedicated initial anchors (the pattern
+# variants of Sec. 2 and the generalization named after Def. 2).
+VARIANTS = [
+    (L.WINDOW_BASIC, 1, 0), (L.WINDOW_ADAPTIVE, 1, 0), (L.WINDOW_EXPANDED, 1, 0),
+    (L.WINDOW_EXPANDED, 0, 0), (L.WINDOW_BASIC, 0, 0), (L.WINDOW_EXPANDED, 1, 1),
+    (L.WINDOW_EXPANDED, 1, 2),
+]
+
+
+@pytest.mark.parametrize("mode,rotate,extra", VARIANTS)
+def test_pattern_variant_attention_parity(mode, rotate, extra):
+    """Block form against the block oracle and token-exact form against Eq. 2,
+    on a straddling shape with a ragged last block, for each pattern variant;
+    the device builder equals the oracle for the variant's CSR."""
+    T, P, B, H = 10, 200, 128, 2
+    N = T * P
+    print(f"[pattern] mode {mode} rotate {rotate} extra {extra}", flush=True)
+    q, k, v = make_qkv(H, N, seed=40 + mode)
+    qd, kd, vd = (x.cuda() for x in (q, k, v))
+    qf, kf, vf = (x.float().numpy() for x in (q, k, v))
+    p = L.Params(window=1, tper=3, window_mode=mode, rotate=rotate, extra_anchors=extra)
+    for s in (1, 2):
+        kw = _kw(p)
+        rp, ci = M.build_mask(T, P, B, s, **kw)
+        drp, dci, _ = _device_csr(T, P, B, s, p)
+        assert drp == rp and dci == ci
+        csr = L.build_mask(T, P, B, s, p, exact=True)
+        csr.upload()
+        blk = L.attention(qd, kd, vd, csr.device_mask())
+        ex = L.attention_exact(qd, kd, vd, csr.exact_mask())
+        torch.cuda.synchronize()
+        ref = OA.assemble(OA.block_sparse_attention(qf, kf, vf, rp, ci, B), H, N, 128, B)
+        err = np.abs(blk.float().cpu().numpy() - ref)
+        assert_close(float(err.max()), float(err.mean()))
+        _, _, A = M.attended_frames(T, s, W=1, tper=3, mode=mode, rotate=bool(rotate),
+                                    extra=extra)
+        fref = OA.frame_sparse_attention(qf, kf, vf, A, P)
+        err = np.abs(ex.float().cpu().numpy() - fref)
+        assert_close(float(err.max()), float(err.mean()))
