@@ -117,6 +117,30 @@ def frame_sparse_rows(q, k, v, A, P, heads, rows, dtype=np.float32):
     return out
 
 
+def text_sparse_rows(q, k, v, A, T, P, heads, rows, dtype=np.float32):
+    """Eq. 2 with text tokens after the T*P video tokens, on selected query
+    rows: a video query (i < T*P) takes the keys of the frames in A(frame i)
+    plus every text key; a text query takes every key.  q, k, v: [H, N, d]
+    with N = T*P + L.  Returns {h: [len(rows), d]}."""
+    V = T * P
+    N = q.shape[1]
+    text_keys = np.arange(V, N)
+    out = {}
+    for h in heads:
+        res = []
+        for i in rows:
+            if i >= V:
+                keys = np.arange(N)
+            else:
+                keys = np.concatenate([np.arange(tau * P, (tau + 1) * P)
+                                       for tau in sorted(A[i // P])] + [text_keys])
+            res.append(attend(np.asarray(q[h, i:i + 1], dtype=dtype),
+                              np.asarray(k[h, keys], dtype=dtype),
+                              np.asarray(v[h, keys], dtype=dtype))[0])
+        out[h] = np.stack(res)
+    return out
+
+
 def assemble(blocks, H, N, d, block, dtype=np.float32):
     """Scatter {(h, qb): rows} from block_sparse_attention into [H, N, d]."""
     out = np.zeros((H, N, d), dtype=dtype)

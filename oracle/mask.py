@@ -28,6 +28,9 @@ Readings where the paper is silent (each is listed in the design notes):
     of the query block and some token of the key block belong to an attended
     frame pair (any-overlap superset of Eq. 2; equal to it when B divides P).
   * Blocks are ceil(N / B); the last one may be ragged.
+  * Text tokens (``text`` = L, dual-stream models): L tokens after the T*P
+    video tokens; they attend to every token and every token attends to
+    them (the paper says only that they join self-attention).
   * Dedicated initial anchors (``extra``, the generalization named after
     Def. 2) are frames 0..extra-1 added to G; they count as global frames in
     Alg. 1 and come out of the budget before the period is derived.
@@ -163,6 +166,45 @@ def token_mask(A, T, P):
                    np.ones((P, P), dtype=bool))
 
 
+def token_mask_text(A, T, P, L):
+    """Eq. 2 with L text tokens appended after the T*P video tokens (a
+    dual-stream model, whose text-encoder tokens join self-attention): video
+    query i keeps video key j iff frame(j) in A(frame(i)); every pair with a
+    text query or a text key is kept.  N x N numpy bool, N = T*P + L."""
+    import numpy as np
+    V = T * P
+    N = V + L
+    m = np.ones((N, N), dtype=bool)
+    m[:V, :V] = token_mask(A, T, P)
+    return m
+
+
+def block_frames_text(b, T, P, B, L):
+    """Segments touched by block b with text: frames 0..T-1 for video tokens,
+    segment T for the text tokens T*P .. T*P+L-1."""
+    N = T * P + L
+    first = min((b * B) // P, T)
+    last = min((min((b + 1) * B, N) - 1) // P, T)
+    return range(first, last + 1)
+
+
+def block_keep_text(A, T, P, B, L):
+    """Block rule with text tokens (any-overlap, as block_keep): keep
+    (qb, kb) iff qb touches text, or kb touches text, or some frame pair of
+    the two blocks is attended."""
+    import numpy as np
+    N = T * P + L
+    nb = ceil_div(N, B)
+    F = np.zeros((nb, T + 1), dtype=np.int64)
+    for b in range(nb):
+        for seg in block_frames_text(b, T, P, B, L):
+            F[b, seg] = 1
+    Mx = np.ones((T + 1, T + 1), dtype=np.int64)
+    Mx[:T, :T] = np.array(frame_mask(A, T), dtype=np.int64)
+    K = (F @ Mx @ F.T) > 0
+    return [[int(kb) for kb in np.nonzero(K[qb])[0]] for qb in range(nb)]
+
+
 def block_keep_bruteforce(A, T, P, B):
     """Kept (q-block, kv-block) pairs by brute force over token pairs.
 
@@ -241,12 +283,14 @@ def to_csr(rows):
 
 
 def build_mask(T, P, B, s, C=21, W=6, tper=0, mode=WINDOW_EXPANDED,
-               rotate=True, tie_high=False, layer=0, extra=0):
+               rotate=True, tie_high=False, layer=0, extra=0, text=0):
     """The whole LVSA mask for one denoising step: (row_ptr, col_idx).
 
     ``layer`` is accepted and ignored: the paper's pattern is the same for
-    every layer and head.
+    every layer and head.  ``text`` text tokens follow the video tokens.
     """
     del layer
     _, _, A = attended_frames(T, s, C, W, tper, mode, rotate, tie_high, extra)
+    if text:
+        return to_csr(block_keep_text(A, T, P, B, text))
     return to_csr(block_keep_incidence(A, T, P, B))

@@ -198,3 +198,24 @@ def test_block_rule_differs_from_eq2_beyond_the_gpu_tolerance():
     frm = OA.frame_sparse_attention(q, k, v, A, P)
     d = np.abs(blk - frm)
     assert d.max() > 2e-2 and d.mean() > 2e-3
+
+
+@pytest.mark.parametrize("L", [1, 5, 13])
+def test_text_rows_match_library_sdpa(L):
+    """Video and text queries with text tokens after the video: equals SDPA
+    (float64) under the token mask written from the rule (text pairs kept,
+    video pairs by frame)."""
+    T, P, d = 4, 5, 8
+    V = T * P
+    N = V + L
+    _, _, A = M.attended_frames(T, 2, W=0, tper=3)
+    q, k, v = _rand((2, N, d), 40 + L), _rand((2, N, d), 41), _rand((2, N, d), 42)
+    allowed = np.array([[i >= V or j >= V or (j // P) in A[i // P] for j in range(N)]
+                        for i in range(N)])
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v),
+        attn_mask=torch.from_numpy(allowed)).numpy()
+    rows = list(range(N))
+    got = OA.text_sparse_rows(q, k, v, A, T, P, [0, 1], rows, dtype=np.float64)
+    for h in (0, 1):
+        np.testing.assert_allclose(got[h], want[h], rtol=0, atol=1e-12)

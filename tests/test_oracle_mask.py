@@ -346,3 +346,37 @@ def test_extra_anchors_invariants(E):
                             assert len(A[t]) <= C
     with pytest.raises(ValueError):
         M.anchor_period(21, 14, 6, extra=1)   # C - (2W+1) - E = 0
+
+
+# ------------------------------------------------------- text tokens ---
+
+@pytest.mark.parametrize("T,P,L", [(4, 3, 5), (5, 4, 1), (3, 6, 11), (6, 2, 0)])
+def test_text_token_mask_elementwise(T, P, L):
+    """Text tokens after the video: every pair touching a text token is
+    kept, video pairs follow Eq. 2; checked element by element."""
+    _, _, A = M.attended_frames(T, 1, W=0, tper=3)
+    tm = M.token_mask_text(A, T, P, L)
+    V = T * P
+    for i in range(V + L):
+        for j in range(V + L):
+            want = i >= V or j >= V or ((j // P) in A[i // P])
+            assert bool(tm[i, j]) == want, (i, j)
+
+
+@pytest.mark.parametrize("T,P,B,L", [(5, 7, 4, 3), (6, 5, 3, 9), (4, 6, 4, 1),
+                                     (7, 3, 2, 6), (5, 8, 8, 8), (4, 9, 4, 0)])
+def test_text_block_rule_is_smallest_cover(T, P, B, L):
+    """The text block rule keeps exactly the blocks holding at least one kept
+    token pair of the text token mask; with L = 0 it is the video rule."""
+    for s in range(3):
+        _, _, A = M.attended_frames(T, s, W=1, tper=3)
+        tm = M.token_mask_text(A, T, P, L)
+        N = T * P + L
+        nb = M.ceil_div(N, B)
+        rows = M.block_keep_text(A, T, P, B, L)
+        for qb in range(nb):
+            for kb in range(nb):
+                tile = tm[qb * B:min((qb + 1) * B, N), kb * B:min((kb + 1) * B, N)]
+                assert (kb in rows[qb]) == bool(tile.any()), (s, qb, kb)
+        if L == 0:
+            assert rows == M.block_keep(A, T, P, B)
