@@ -48,6 +48,13 @@ def kept_flops(row_ptr, col_idx, n_tokens, block, heads, d=128):
     return 4.0 * d * heads * float((rows * per_row).sum())
 
 
+def eq2_pairs(frames_per_query, P, text, n_tokens):
+    """(query, key) token pairs of Eq. 2: P*P per attended frame pair, plus
+    every pair with a text query or a text key."""
+    video = P * P * sum(frames_per_query)
+    return float(video + (n_tokens - text) * text + text * n_tokens)
+
+
 def median(xs):
     xs = sorted(xs)
     return xs[len(xs) // 2]
@@ -96,7 +103,8 @@ def cpu_baseline(w, target_s):
         cores = os.cpu_count()
     t0 = time.perf_counter()
     rp, ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, 10,
-                          C=w.budget_frames, W=w.window, tper=w.tper)
+                          C=w.budget_frames, W=w.window, tper=w.tper,
+                          text=w.text_tokens)
     mask_s = time.perf_counter() - t0
     q, k, v = make_qkv(1, w.n_tokens, value_scale=w.value_scale)
     q, k, v = (x.float().numpy() for x in (q, k, v))
@@ -154,7 +162,8 @@ def main():
     from paper_2605_31057_amd.inputs import WORKLOADS, workload_qkv
 
     w = WORKLOADS[args.workload]
-    params = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    params = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
+                      text_tokens=w.text_tokens)
     print(f"[bench] {w.name}: generating inputs", file=sys.stderr, flush=True)
     q, k, v = (x.cuda() for x in workload_qkv(w))
     out = torch.empty_like(q)
@@ -245,7 +254,8 @@ def main():
         _, anc, lo, hi = L.frame_sets(w.frames, s_ref, params)
         per_frame = [len(set(anc) | set(range(lo[t], hi[t] + 1)))
                      for t in range(w.frames)]
-        eq2_flops = 4.0 * 128 * w.heads * w.tokens_per_frame ** 2 * sum(per_frame)
+        eq2_flops = 4.0 * 128 * w.heads * eq2_pairs(per_frame, w.tokens_per_frame,
+                                                    w.text_tokens, w.n_tokens)
         host_ex = []
         for _ in range(5):
             t0 = time.perf_counter()
@@ -276,7 +286,8 @@ def main():
                                     (L.WINDOW_BASIC, 1, 0), (L.WINDOW_EXPANDED, 0, 0),
                                     (L.WINDOW_EXPANDED, 1, 1)]:
             pv = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
-                          window_mode=mode, rotate=rotate, extra_anchors=extra)
+                          window_mode=mode, rotate=rotate, extra_anchors=extra,
+                          text_tokens=w.text_tokens)
             csr = L.build_mask(w.frames, w.tokens_per_frame, w.block, s_ref, pv)
             hrp, hci = csr.arrays()
             csr.upload(stream)
@@ -291,7 +302,8 @@ def main():
                 "T_per": tper, "frames_per_query_min": min(sizes),
                 "frames_per_query_max": max(sizes),
                 "block_density": int(hrp[-1]) / (nb * nb),
-                "token_density": sum(sizes) / w.frames ** 2,
+                "token_density": eq2_pairs(sizes, w.tokens_per_frame, w.text_tokens,
+                                           w.n_tokens) / w.n_tokens ** 2,
                 "ms_per_call": v_ms, "tflops_kept": fl / (v_ms * 1e-3) / 1e12,
             })
             csr.free()

@@ -85,10 +85,16 @@ typedef struct lvsa_params {
                             (2W+1) - E)) (needs C > 2W+1+E when tper == 0).
                             E = 1 keeps frame 0 an anchor at every step.
                             Default 0.                                      */
+  int32_t text_tokens;   /* L >= 0 text tokens after the T*P video tokens
+                            (dual-stream models, whose text-encoder tokens
+                            join self-attention, Sec. 3): the mask covers
+                            N = T*P + L tokens; every query attends to every
+                            text token and every text query to every token.
+                            A shorter text is a smaller L.  Default 0.      */
 } lvsa_params;
 
 /* Fills *p with C = 21, W = 6, tper = 0, EXPANDED, rotate = 1, tie_high = 0,
- * extra_anchors = 0.
+ * extra_anchors = 0, text_tokens = 0.
  * C = 21 is the paper's Wan 2.1 budget ((81-1)/4 + 1 frames); the paper does
  * not print W, and 6 is the smallest W that keeps |A(t)| within two frames of
  * C and Alg. 1 within eight iterations on every Wan horizon. */
@@ -114,14 +120,16 @@ lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
 
 /* ---------------------------------------------------------- block CSR ---- */
 
-/* Token i (0 <= i < N = T*P) lies in frame i / P and block i / B; there are
- * nb = ceil(N / B) query blocks and nb key blocks, the last possibly ragged.
- * Query block qb keeps key block kb iff some token of qb and some token of kb
- * lie in frames t, tau with tau in A(t) (Eq. 2 applied to whole blocks: every
- * attended token pair is covered; a block straddling a frame edge brings the
- * rest of its tokens along).  Rows list kb in ascending order, without
- * repeats, and always contain the diagonal block.  The mask does not depend
- * on the head or the layer. */
+/* Token i (0 <= i < N = T*P + L) lies in block i / B and, for i < T*P, in
+ * frame i / P; tokens T*P .. N-1 are the text tokens (segment T, L =
+ * params->text_tokens, usually 0).  There are nb = ceil(N / B) query blocks
+ * and nb key blocks, the last possibly ragged.  Query block qb keeps key
+ * block kb iff some token of qb and some token of kb lie in segments t, tau
+ * with tau in A(t), or with t or tau the text (Eq. 2 applied to whole blocks:
+ * every attended token pair is covered; a block straddling a frame edge
+ * brings the rest of its tokens along).  Rows list kb in ascending order,
+ * without repeats, and always contain the diagonal block.  The mask does not
+ * depend on the head or the layer. */
 typedef struct lvsa_csr lvsa_csr; /* opaque, library-owned */
 
 /* Host builder (the paper builds this metadata on the CPU once per step).
@@ -190,15 +198,17 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
  * It needs P >= B (a block then touches at most two frames), B <= 255 and
  * nb <= 65536.
  *
- * Entry word (uint32) of kept pair (qb, kb); f0 <= f1 are the frames touched
- * by qb, g0 <= g1 those touched by kb (equal when the block lies in one frame):
+ * Entry word (uint32) of kept pair (qb, kb); f0 <= f1 are the segments
+ * (frames, or T for the text tokens) touched by qb, g0 <= g1 those touched by
+ * kb (equal when the block lies in one segment); "frame T is in A(t)" and
+ * "frame tau is in A(T)" hold for every t, tau:
  *   bits  0..15  kb
- *   bits 16..23  kfirst: tokens of kb in frame g0 (B when g0 == g1)
+ *   bits 16..23  kfirst: tokens of kb in segment g0 (B when g0 == g1)
  *   bits 24..27  pattern: bit 2a+b set iff frame (b ? g1 : g0) is in
  *                A(a ? f1 : f0)
  *   bits 28..31  zero
  * Query token i of qb attends key token j of kb iff pattern bit
- * 2*(frame(i) != f0) + (frame(j) != g0) is set. */
+ * 2*(segment(i) != f0) + (segment(j) != g0) is set. */
 typedef struct lvsa_exact_mask {
   int32_t n_tokens;        /* N = T*P                                       */
   int32_t block;           /* B                                             */

@@ -48,15 +48,15 @@ class LvsaError(RuntimeError):
 
 class Params(ctypes.Structure):
     """lvsa_params: C, W, T_per override, window rule, rotation, tie rule,
-    dedicated initial anchors."""
+    dedicated initial anchors, text tokens after the video tokens."""
     _fields_ = [("budget_frames", _i32), ("window", _i32), ("tper", _i32),
                 ("window_mode", _i32), ("rotate", _i32), ("tie_high", _i32),
-                ("extra_anchors", _i32)]
+                ("extra_anchors", _i32), ("text_tokens", _i32)]
 
     def __init__(self, **kw):
         d = dict(budget_frames=21, window=6, tper=0,
                  window_mode=WINDOW_EXPANDED, rotate=1, tie_high=0,
-                 extra_anchors=0)
+                 extra_anchors=0, text_tokens=0)
         d.update(kw)
         super().__init__(**{k: int(v) for k, v in d.items()})
 
@@ -266,7 +266,7 @@ def build_mask_device(T, P, B, step, row_ptr, col_idx, params=None, layer=0,
                                         _p(row_ptr.data_ptr()), _p(col_idx.data_ptr()),
                                         col_idx.numel(), _stream_ptr(stream)),
            "lvsa_build_mask_device")
-    return device_mask(T * P, B, row_ptr, col_idx)
+    return device_mask(T * P + params.text_tokens, B, row_ptr, col_idx)
 
 
 def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
@@ -278,8 +278,9 @@ def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
         T, P, B, step, layer, ctypes.byref(params), _p(row_ptr.data_ptr()),
         _p(entry.data_ptr()), entry.numel(), _stream_ptr(stream)),
         "lvsa_build_exact_mask_device")
-    nb = (T * P + B - 1) // B
-    return ExactMask(T * P, B, nb, P, row_ptr.data_ptr(), entry.data_ptr())
+    N = T * P + params.text_tokens
+    nb = (N + B - 1) // B
+    return ExactMask(N, B, nb, P, row_ptr.data_ptr(), entry.data_ptr())
 
 
 def _tensor(t):

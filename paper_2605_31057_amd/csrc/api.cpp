@@ -18,6 +18,7 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
     return LVSA_EINVAL;
   if (p->tper < 0) return LVSA_EINVAL;
   if (p->extra_anchors < 0 || p->extra_anchors > LVSA_MAX_FRAMES) return LVSA_EINVAL;
+  if (p->text_tokens < 0) return LVSA_EINVAL;
   int32_t tper = p->tper;
   if (tper == 0) {
     // Sec. 2, budget paragraph: T_per = ceil(T / (C - (2W+1))), for C > 2W+1;
@@ -37,15 +38,16 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
   c.rotate = p->rotate;
   c.tie_high = p->tie_high;
   c.extra = p->extra_anchors;
+  c.text = p->text_tokens;
   c.g = 0;
   for (int32_t f = 0; f < T; ++f) c.g += is_anchor(c, f) ? 1 : 0;
   *out = c;
   return LVSA_OK;
 }
 
-lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B) {
-  if (T < 1 || P < 1 || B < 1 || B > (1 << 20)) return LVSA_EINVAL;
-  const int64_t N = (int64_t)T * P;
+lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B, int32_t L) {
+  if (T < 1 || P < 1 || B < 1 || B > (1 << 20) || L < 0) return LVSA_EINVAL;
+  const int64_t N = (int64_t)T * P + L;
   if (N + B > INT32_MAX) return LVSA_EINVAL;
   const int64_t nb = (N + B - 1) / B;
   if (nb * nb > INT32_MAX) return LVSA_EINVAL;  // nnz must fit row_ptr
@@ -85,7 +87,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 10200; }
+int32_t lvsa_version(void) { return 10300; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
@@ -96,6 +98,7 @@ void lvsa_params_default(lvsa_params* p) {
   p->rotate = 1;
   p->tie_high = 0;
   p->extra_anchors = 0;
+  p->text_tokens = 0;
 }
 
 lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
@@ -130,12 +133,12 @@ lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
   if (!out) return LVSA_EINVAL;
   *out = nullptr;
   if (layer < 0) return LVSA_EINVAL;
-  lvsa_status st = check_mask_shape(T, P, B);
-  if (st != LVSA_OK) return st;
   FrameCfg c;
-  st = resolve_frames(T, step, p, &c);
+  lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
-  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  st = check_mask_shape(T, P, B, c.text);
+  if (st != LVSA_OK) return st;
+  const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (exact && !exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
   lvsa_csr* h = new (std::nothrow) lvsa_csr();
   if (!h) return LVSA_ENOMEM;
@@ -147,7 +150,7 @@ lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
     delete h;
     return LVSA_ENOMEM;
   }
-  h->n_tokens = T * P;
+  h->n_tokens = (int32_t)mask_tokens(c, P);
   h->frame_tokens = P;
   h->block = B;
   h->n_blocks = (int32_t)h->row_ptr.size() - 1;
@@ -279,12 +282,12 @@ lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
                                          int32_t* d_row_ptr, uint32_t* d_entry,
                                          int64_t entry_capacity, void* stream) {
   if (layer < 0 || !d_row_ptr || !d_entry) return LVSA_EINVAL;
-  lvsa_status st = check_mask_shape(T, P, B);
-  if (st != LVSA_OK) return st;
   FrameCfg c;
-  st = resolve_frames(T, step, p, &c);
+  lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
-  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  st = check_mask_shape(T, P, B, c.text);
+  if (st != LVSA_OK) return st;
+  const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (!exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
   if (entry_capacity < nb * nb) return LVSA_EINVAL;
   if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry,
@@ -299,12 +302,12 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t* d_col_idx, int64_t col_capacity,
                                    void* stream) {
   if (layer < 0 || !d_row_ptr || !d_col_idx) return LVSA_EINVAL;
-  lvsa_status st = check_mask_shape(T, P, B);
-  if (st != LVSA_OK) return st;
   FrameCfg c;
-  st = resolve_frames(T, step, p, &c);
+  lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
-  const int64_t nb = ((int64_t)T * P + B - 1) / B;
+  st = check_mask_shape(T, P, B, c.text);
+  if (st != LVSA_OK) return st;
+  const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (col_capacity < nb * nb) return LVSA_EINVAL;
   if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr,
                                (hipStream_t)stream) != hipSuccess)
@@ -389,8 +392,7 @@ lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  const lvsa_exact_mask* mask, lvsa_tensor* out,
                                  void* stream) {
   if (!mask || !mask->row_ptr || !mask->entry) return LVSA_EINVAL;
-  if (mask->frame_tokens < 1 || mask->n_tokens % mask->frame_tokens != 0)
-    return LVSA_EINVAL;
+  if (mask->frame_tokens < 1) return LVSA_EINVAL;
   if (!exact_supported(mask->frame_tokens, mask->block, mask->n_blocks))
     return LVSA_EUNSUPPORTED;
   return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,

@@ -19,6 +19,7 @@ struct FrameCfg {
   int32_t k;         // Eq. 3 anchors ceil(T / T_per)
   int32_t extra;     // dedicated initial anchors: frames 0..extra-1
   int32_t g;         // |G|: Eq. 3 (or Def. 2) anchors plus the extra ones
+  int32_t text;      // text tokens after the T*P video tokens (segment T)
   int32_t s0;        // s mod T_per (0 for fixed anchors)
   int32_t mode;      // LVSA_WINDOW_*
   int32_t rotate;    // Eq. 3 (1) or Def. 2's fixed set (0)
@@ -87,21 +88,34 @@ __host__ __device__ inline int32_t frame_window(const FrameCfg& c, int32_t t,
   return steps;
 }
 
-// First and last frame touched by block b (tokens b*B .. min((b+1)*B, N)-1).
-__host__ __device__ inline void block_frame_range(int32_t b, int32_t P,
-                                                  int32_t B, int32_t N,
-                                                  int32_t* first,
+// First and last segment touched by block b (tokens b*B .. min((b+1)*B, N)-1):
+// frames 0..T-1 for video tokens, segment T for the text tokens after them.
+__host__ __device__ inline void block_frame_range(int32_t b, int32_t T,
+                                                  int32_t P, int32_t B,
+                                                  int32_t N, int32_t* first,
                                                   int32_t* last) {
   const int64_t t0 = (int64_t)b * B;
   const int64_t end = t0 + B < (int64_t)N ? t0 + B : (int64_t)N;
-  *first = (int32_t)(t0 / P);
-  *last = (int32_t)((end - 1) / P);
+  *first = (int32_t)(t0 / P < T ? t0 / P : T);
+  *last = (int32_t)((end - 1) / P < T ? (end - 1) / P : T);
+}
+
+// Key blocks of segment tau: frame tau's tokens tau*P .. tau*P+P-1, or the
+// text tokens T*P .. N-1 for tau = T.
+__host__ __device__ inline void segment_blocks(int32_t tau, int32_t T, int32_t P,
+                                               int32_t B, int32_t N, int32_t* b0,
+                                               int32_t* b1) {
+  const int64_t first = (int64_t)tau * P;
+  const int64_t last = tau < T ? first + P - 1 : (int64_t)N - 1;
+  *b0 = (int32_t)(first / B);
+  *b1 = (int32_t)(last / B);
 }
 
 // Token-exact entry word of a kept block pair (lvsa.h, "token-exact form").
-// The query block touches frames f0..f1 and key block kb frames g0..g1, each
-// at most two frames apart since P >= B; kb's first kfirst tokens lie in g0.
-// attends(t, tau) is tau in A(t).
+// The query block touches segments f0..f1 and key block kb segments g0..g1,
+// each at most two apart since P >= B (segment T, the text tokens, follows
+// frame T-1); kb's first kfirst tokens lie in g0.  attends(t, tau) is
+// "segment tau is attended by segment t": tau in A(t), or either is text.
 //   bits  0..15  kb
 //   bits 16..23  kfirst (B when kb lies in one frame)
 //   bits 24..27  bit 2a+b: frame (b ? g1 : g0) is in A(a ? f1 : f0)
@@ -115,24 +129,24 @@ __host__ __device__ inline uint32_t exact_word(int32_t kb, int32_t g0,
   return (uint32_t)kb | (kfirst << 16) | (pat << 24);
 }
 
-// Frames g0..g1 of key block kb and its tokens in frame g0 (B if g0 == g1).
-__host__ __device__ inline void key_block_split(int32_t kb, int32_t P,
-                                                int32_t B, int32_t N,
+// Segments g0..g1 of key block kb and its tokens in g0 (B if g0 == g1).
+__host__ __device__ inline void key_block_split(int32_t kb, int32_t T,
+                                                int32_t P, int32_t B, int32_t N,
                                                 int32_t* g0, int32_t* g1,
                                                 uint32_t* kfirst) {
-  block_frame_range(kb, P, B, N, g0, g1);
+  block_frame_range(kb, T, P, B, N, g0, g1);
   *kfirst = *g1 > *g0 ? (uint32_t)((int64_t)(*g0 + 1) * P - (int64_t)kb * B)
                       : (uint32_t)B;
 }
 
 template <typename Attends>
 __host__ __device__ inline uint32_t exact_entry(int32_t kb, int32_t f0,
-                                                int32_t f1, int32_t P,
-                                                int32_t B, int32_t N,
+                                                int32_t f1, int32_t T,
+                                                int32_t P, int32_t B, int32_t N,
                                                 const Attends& attends) {
   int32_t g0, g1;
   uint32_t kfirst;
-  key_block_split(kb, P, B, N, &g0, &g1, &kfirst);
+  key_block_split(kb, T, P, B, N, &g0, &g1, &kfirst);
   return exact_word(kb, g0, g1, kfirst, f0, f1, attends);
 }
 

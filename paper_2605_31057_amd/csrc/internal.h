@@ -15,8 +15,14 @@ namespace lvsa {
 lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
                            FrameCfg* out);
 
-// Checks (T, P, B) of a block mask: T*P + B must fit in int32.
-lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B);
+// Checks (T, P, B, text tokens L) of a block mask: N = T*P + L, N + B must fit
+// in int32 and nb*nb too.
+lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B, int32_t L);
+
+// Tokens of the mask: T*P video tokens and the text tokens after them.
+__host__ __device__ inline int64_t mask_tokens(const FrameCfg& c, int32_t P) {
+  return (int64_t)c.T * P + c.text;
+}
 
 // Host CSR construction (mask_host.cpp).  `entry` (may be null) receives the
 // token-exact entry word of every kept block; callers pass it only when

@@ -25,22 +25,24 @@ struct Rows {
   const uint8_t* anchor;
   const int16_t* lo;
   const int16_t* hi;
-  int32_t T, P, B, N;
+  int32_t T, P, B, N, S;   // S segments: T frames, plus the text if any
 };
 
-// Visits the kept key blocks of query block qb in ascending order.
+// Visits the kept key blocks of query block qb in ascending order.  Text
+// (segment T) is attended by every query; a query block touching the text
+// attends to every segment.
 template <typename F>
 __device__ inline void for_each_kept(const Rows& r, int32_t qb, F&& emit) {
   int32_t f0, f1;
-  block_frame_range(qb, r.P, r.B, r.N, &f0, &f1);
+  block_frame_range(qb, r.T, r.P, r.B, r.N, &f0, &f1);
   int32_t last = -1;
-  for (int32_t tau = 0; tau < r.T; ++tau) {
-    bool att = r.anchor[tau] != 0;
+  for (int32_t tau = 0; tau < r.S; ++tau) {
+    bool att = tau == r.T || f1 == r.T || r.anchor[tau] != 0;
     for (int32_t t = f0; t <= f1 && !att; ++t)
       att = r.lo[t] <= tau && tau <= r.hi[t];
     if (!att) continue;
-    const int32_t b0 = (int32_t)((int64_t)tau * r.P / r.B);
-    const int32_t b1 = (int32_t)(((int64_t)tau * r.P + r.P - 1) / r.B);
+    int32_t b0, b1;
+    segment_blocks(tau, r.T, r.P, r.B, r.N, &b0, &b1);
     for (int32_t b = imax(b0, last + 1); b <= b1; ++b) emit(b);
     last = imax(last, b1);
   }
@@ -57,7 +59,7 @@ __global__ __launch_bounds__(kThreads) void build_mask_kernel(
 
   const int32_t tid = threadIdx.x;
   const int32_t T = c.T;
-  const int32_t N = T * P;
+  const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
 
   for (int32_t t = tid; t < T; t += kThreads) {
@@ -73,7 +75,7 @@ __global__ __launch_bounds__(kThreads) void build_mask_kernel(
   }
   __syncthreads();
 
-  const Rows r{s_anchor, s_lo, s_hi, T, P, B, N};
+  const Rows r{s_anchor, s_lo, s_hi, T, P, B, N, c.text > 0 ? T + 1 : T};
   for (int32_t qb = tid; qb < nb; qb += kThreads) {
     int32_t n = 0;
     for_each_kept(r, qb, [&](int32_t) { ++n; });
@@ -100,16 +102,16 @@ __global__ __launch_bounds__(kThreads) void build_mask_kernel(
   }
 
   auto attends = [&](int32_t t, int32_t tau) {
-    return s_anchor[tau] != 0 || (s_lo[t] <= tau && tau <= s_hi[t]);
+    return t == T || tau == T || s_anchor[tau] != 0 || (s_lo[t] <= tau && tau <= s_hi[t]);
   };
   for (int32_t qb = tid; qb < nb; qb += kThreads) {
     const int32_t beg = row_ptr[qb];
     int32_t f0, f1;
-    block_frame_range(qb, P, B, N, &f0, &f1);
+    block_frame_range(qb, T, P, B, N, &f0, &f1);
     int32_t n = 0;
     for_each_kept(r, qb, [&](int32_t b) {
       if (col_idx) col_idx[beg + n] = b;
-      if (entry) entry[beg + n] = exact_entry(b, f0, f1, P, B, N, attends);
+      if (entry) entry[beg + n] = exact_entry(b, f0, f1, T, P, B, N, attends);
       ++n;
     });
   }

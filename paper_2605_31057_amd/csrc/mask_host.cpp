@@ -6,12 +6,16 @@
 // and some frame tau touched by kb have tau in A(t), where
 // A(t) = G^s U [lo(t), hi(t)].
 //
-// For each query block the attended frames are gathered into a T-entry
-// flag array, then each attended frame contributes its block range
+// For each query block the attended frames are gathered into a flag array,
+// then each attended frame contributes its block range
 // [tau*P/B, ((tau+1)*P-1)/B]; ranges come in ascending order and overlap only
 // at a shared straddling block, so a running "last emitted" index keeps the
 // row ascending and free of repeats.  Consecutive query blocks that touch
 // the same frames have identical rows, which are copied.
+//
+// Text tokens (dual-stream models) follow the video tokens as one more
+// segment T: every query attends to them and a query block touching them
+// attends to every segment.
 //
 // The token-exact entry words (lvsa.h) are built alongside when asked for:
 // one word per kept block, from the two (at most) frames of each side.
@@ -27,8 +31,9 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<int32_t>* col_idx,
                     std::vector<uint32_t>* entry) {
   const int32_t T = c.T;
-  const int32_t N = T * P;
+  const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
+  const int32_t S = c.text > 0 ? T + 1 : T;   // segments: frames, then text
   std::vector<int32_t> lo(T), hi(T);
   std::vector<uint8_t> anchor(T);
   for (int32_t t = 0; t < T; ++t) {
@@ -36,7 +41,7 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
     frame_window(c, t, &lo[t], &hi[t]);
   }
   auto attends = [&](int32_t t, int32_t tau) {
-    return anchor[tau] != 0 || (lo[t] <= tau && tau <= hi[t]);
+    return t == T || tau == T || anchor[tau] != 0 || (lo[t] <= tau && tau <= hi[t]);
   };
   // Per key block: its frames and split point, so an entry word costs four
   // table lookups.
@@ -47,7 +52,7 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
     kg1.resize(nb);
     kfirst.resize(nb);
     for (int32_t b = 0; b < nb; ++b)
-      key_block_split(b, P, B, N, &kg0[b], &kg1[b], &kfirst[b]);
+      key_block_split(b, T, P, B, N, &kg0[b], &kg1[b], &kfirst[b]);
   }
 
   // Pass 1: the distinct rows (one per run of query blocks touching the same
@@ -56,22 +61,27 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
   std::vector<uint32_t> uniq_e;
   std::vector<int64_t> src(nb);
   row_ptr->assign(nb + 1, 0);
-  std::vector<uint8_t> attended(T);
+  std::vector<uint8_t> attended(S);
   int32_t prev_first = -1, prev_last = -1;
   int64_t prev_begin = 0, prev_len = 0;
   for (int32_t qb = 0; qb < nb; ++qb) {
     int32_t f0, f1;
-    block_frame_range(qb, P, B, N, &f0, &f1);
+    block_frame_range(qb, T, P, B, N, &f0, &f1);
     if (f0 != prev_first || f1 != prev_last) {
       prev_begin = (int64_t)uniq.size();
-      std::memcpy(attended.data(), anchor.data(), T);
-      for (int32_t t = f0; t <= f1; ++t)
-        std::fill(attended.begin() + lo[t], attended.begin() + hi[t] + 1, 1);
+      if (f1 == T) {
+        std::fill(attended.begin(), attended.end(), 1);   // text queries: all
+      } else {
+        std::memcpy(attended.data(), anchor.data(), T);
+        for (int32_t t = f0; t <= f1; ++t)
+          std::fill(attended.begin() + lo[t], attended.begin() + hi[t] + 1, 1);
+        if (S > T) attended[T] = 1;                       // text keys: all
+      }
       int32_t last = -1;
-      for (int32_t tau = 0; tau < T; ++tau) {
+      for (int32_t tau = 0; tau < S; ++tau) {
         if (!attended[tau]) continue;
-        const int32_t b0 = (int32_t)((int64_t)tau * P / B);
-        const int32_t b1 = (int32_t)(((int64_t)tau * P + P - 1) / B);
+        int32_t b0, b1;
+        segment_blocks(tau, T, P, B, N, &b0, &b1);
         for (int32_t b = std::max(b0, last + 1); b <= b1; ++b) {
           uniq.push_back(b);
           if (entry)

@@ -28,12 +28,13 @@ class Workload:
     steps: tuple = (10,)  # denoising steps the mask is built for
     layers: tuple = (0,)
     value_scale: float = 1.0
+    text_tokens: int = 0   # text tokens after the video tokens (dual-stream)
     desc: str = ""
     extra: dict = field(default_factory=dict)
 
     @property
     def n_tokens(self):
-        return self.frames * self.tokens_per_frame
+        return self.frames * self.tokens_per_frame + self.text_tokens
 
     @property
     def n_blocks(self):
@@ -68,6 +69,12 @@ WORKLOADS = {
     "hv15_2x": Workload("hv15_2x", 16, 65, 1590, 128, budget_frames=33, window=6,
                         steps=tuple(range(50)), layers=(0, 1, 2, 3),
                         desc="HunyuanVideo-1.5 layer, 65 x 30x53 tokens, 16 heads"),
+    # The same layer with the dual-stream text tokens in self-attention: 512
+    # text tokens (prompts of about 500 tokens) after the video tokens.
+    "hv15_2x_text": Workload("hv15_2x_text", 16, 65, 1590, 128, budget_frames=33,
+                             window=6, steps=(0, 10), text_tokens=512,
+                             desc="HunyuanVideo-1.5 layer, 65 x 30x53 video + 512 "
+                                  "text tokens, 16 heads"),
 }
 
 

@@ -13,7 +13,8 @@ MEAN_ABS = 2e-3
 
 def oracle_csr(w, step, layer=0):
     return M.build_mask(w.frames, w.tokens_per_frame, w.block, step,
-                        C=w.budget_frames, W=w.window, tper=w.tper, layer=layer)
+                        C=w.budget_frames, W=w.window, tper=w.tper, layer=layer,
+                        text=w.text_tokens)
 
 
 def sample_q_blocks(row_ptr, T, P, B, n_random=2, seed=0):

@@ -47,12 +47,15 @@ def test_status_strings_and_version():
 
 def _oracle_kw(p):
     return dict(C=p.budget_frames, W=p.window, tper=p.tper, mode=p.window_mode,
-                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors)
+                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors,
+                text=p.text_tokens)
 
 
 def _check_frames(T, s, p):
     tper, anchors, lo, hi = L.frame_sets(T, s, p)
-    T_per, G, A = M.attended_frames(T, s, **_oracle_kw(p))
+    kw = _oracle_kw(p)
+    kw.pop("text")   # text tokens do not change the frame sets
+    T_per, G, A = M.attended_frames(T, s, **kw)
     assert tper == T_per
     assert anchors == sorted(G)
     for t in range(T):
@@ -65,14 +68,15 @@ def _check_csr(T, P, B, s, p, layer=0):
     want_rp, want_ci = M.build_mask(T, P, B, s, layer=layer, **_oracle_kw(p))
     assert row_ptr.tolist() == want_rp
     assert col_idx.tolist() == want_ci
-    assert csr.n_tokens == T * P and csr.block == B
+    assert csr.n_tokens == T * P + p.text_tokens and csr.block == B
     csr.free()
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
 def test_host_builder_matches_oracle_on_workloads(name):
     w = WORKLOADS[name]
-    p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
+                 text_tokens=w.text_tokens)
     T_per = M.anchor_period(w.frames, w.budget_frames, w.window, w.tper)
     steps = sorted(set(range(T_per)) | set(w.steps[:3]) | {T_per + 1})
     for s in steps:
@@ -225,25 +229,26 @@ def test_attention_rejects_before_launch():
 
 # ------------------------------------------------------ token-exact form ---
 
-def decode_entries(row_ptr, col_idx, entry, T, P, B):
+def decode_entries(row_ptr, col_idx, entry, T, P, B, L=0):
     """Token mask described by the entry words (the token-exact form that
-    include/lvsa.h defines), checking each word's fixed fields on the way."""
-    N = T * P
+    include/lvsa.h defines), checking each word's fixed fields on the way.
+    Segment of a token: its frame, or T for the L text tokens."""
+    N = T * P + L
     nb = -(-N // B)
     tm = np.zeros((N, N), dtype=bool)
-    tok_frame = np.arange(N) // P
+    tok_frame = np.minimum(np.arange(N) // P, T)
     for qb in range(nb):
         rows = np.arange(qb * B, min((qb + 1) * B, N))
-        a = (tok_frame[rows] != (qb * B) // P).astype(np.int64)
+        a = (tok_frame[rows] != tok_frame[qb * B]).astype(np.int64)
         for idx in range(row_ptr[qb], row_ptr[qb + 1]):
             w = int(entry[idx])
             kb = int(col_idx[idx])
             assert w & 0xFFFF == kb and w >> 28 == 0, hex(w)
             kfirst, pat = (w >> 16) & 0xFF, (w >> 24) & 0xF
             cols = np.arange(kb * B, min((kb + 1) * B, N))
-            g0 = (kb * B) // P
+            g0 = tok_frame[kb * B]
             b = (tok_frame[cols] != g0).astype(np.int64)
-            straddles = (min((kb + 1) * B, N) - 1) // P != g0
+            straddles = tok_frame[min((kb + 1) * B, N) - 1] != g0
             assert kfirst == ((g0 + 1) * P - kb * B if straddles else B), (qb, kb)
             assert np.array_equal(b, (cols - kb * B >= kfirst).astype(np.int64))
             bit = 2 * a[:, None] + b[None, :]
@@ -333,10 +338,54 @@ def test_exact_attention_and_builder_reject_before_launch():
     q, k, v, o = _t(0x10000), _t(0x20000), _t(0x30000), _t(0x40000)
     cases = [
         (L.ExactMask(n, 128, nbk, 100, 0x2000, 0x3000), L.EUNSUPPORTED),  # P < B
-        (L.ExactMask(n, 128, nbk, 300, 0x2000, 0x3000), L.EINVAL),    # N % P != 0
+        (L.ExactMask(n, 128, nbk, 0, 0x2000, 0x3000), L.EINVAL),      # P < 1
         (L.ExactMask(n, 128, nbk, 200, 0x2000, 0), L.EINVAL),         # no entries
         (L.ExactMask(n, 96, 11, 200, 0x2000, 0x3000), L.EUNSUPPORTED),  # block
     ]
     for m, want in cases:
         assert lib.lvsa_attention_exact(ref(q), ref(k), ref(v), ref(m), ref(o),
                                         None) == want, (m.frame_tokens, m.block)
+
+
+# ------------------------------------------------------- text tokens ---
+
+TEXT_CASES = [  # T, P, B, L: text after the video, ragged lengths
+    (5, 200, 128, 77), (7, 100, 64, 300), (6, 130, 128, 1), (4, 256, 128, 128),
+    (3, 255, 128, 513),
+]
+
+
+@pytest.mark.parametrize("T,P,B,Lt", TEXT_CASES)
+def test_host_builder_with_text_matches_oracle(T, P, B, Lt):
+    """Block CSR bit for bit against the oracle's text block rule, and the
+    entry words decode to the oracle's text token mask."""
+    for mode, rotate in [(2, 1), (0, 0)]:
+        for s in (0, 2):
+            p = L.Params(budget_frames=0, window=1, tper=3, window_mode=mode,
+                         rotate=rotate, text_tokens=Lt)
+            csr = L.build_mask(T, P, B, s, p, exact=True)
+            row_ptr, col_idx = csr.arrays()
+            kw = dict(W=1, tper=3, mode=mode, rotate=bool(rotate))
+            want_rp, want_ci = M.build_mask(T, P, B, s, text=Lt, **kw)
+            assert row_ptr.tolist() == want_rp and col_idx.tolist() == want_ci
+            assert csr.n_tokens == T * P + Lt
+            _, _, A = M.attended_frames(T, s, **kw)
+            got = decode_entries(row_ptr, col_idx, csr.entries(), T, P, B, Lt)
+            assert np.array_equal(got, M.token_mask_text(A, T, P, Lt)), (mode, s)
+            blk = L.build_mask(T, P, B, s, p)
+            assert all(np.array_equal(x, y) for x, y in zip(blk.arrays(), (row_ptr, col_idx)))
+
+
+def test_host_builder_text_on_hv_horizon():
+    """HunyuanVideo 1.5 at 2x (65 x 30x53, C = 33) with 512 text tokens."""
+    T, P, B, Lt = 65, 1590, 128, 512
+    p = L.Params(budget_frames=33, window=6, text_tokens=Lt)
+    for s in (0, 10):
+        csr = L.build_mask(T, P, B, s, p)
+        row_ptr, col_idx = csr.arrays()
+        want_rp, want_ci = M.build_mask(T, P, B, s, C=33, W=6, text=Lt)
+        assert row_ptr.tolist() == want_rp and col_idx.tolist() == want_ci
+    bad = L.Params(text_tokens=-1)
+    out = ctypes.c_void_p()
+    assert L.lib().lvsa_build_mask(65, 1590, 128, 0, 0, ctypes.byref(bad),
+                                   ctypes.byref(out)) == L.EINVAL

@@ -30,7 +30,8 @@ def _gpu():
 
 
 def _params(w):
-    return L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    return L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
+                    text_tokens=w.text_tokens)
 
 
 def _run_sparse(w, q, k, v, step, out=None):

@@ -25,7 +25,7 @@ def _gpu():
 
 
 def _device_csr(T, P, B, step, p, layer=0):
-    nb = -(-(T * P) // B)
+    nb = -(-(T * P + p.text_tokens) // B)
     rp = torch.full((nb + 1,), -1, dtype=torch.int32, device="cuda")
     ci = torch.full((nb * nb,), -1, dtype=torch.int32, device="cuda")
     L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer)
@@ -37,13 +37,15 @@ def _device_csr(T, P, B, step, p, layer=0):
 
 def _kw(p):
     return dict(C=p.budget_frames, W=p.window, tper=p.tper, mode=p.window_mode,
-                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors)
+                rotate=bool(p.rotate), tie_high=bool(p.tie_high), extra=p.extra_anchors,
+                text=p.text_tokens)
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
 def test_device_builder_matches_oracle_workloads(name):
     w = WORKLOADS[name]
-    p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
+    p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
+                 text_tokens=w.text_tokens)
     steps = list(w.steps) if len(w.steps) > 1 else [0, 1, 10, 17]
     print(f"[mask] {name} steps {steps[0]}..{steps[-1]}", flush=True)
     for s in steps:
