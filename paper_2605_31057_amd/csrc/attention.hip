@@ -12,14 +12,19 @@
 //   keep independent online softmax states over disjoint keys and are merged
 //   once at the end.
 //
-// Pipeline (per wave, one key block per step)
-//   LDS holds two K stages and three V stages (slab layout, see below).  K runs one block ahead of V:
-//   during step j the wave computes S(j+1) = K(j+1) Q^T while it exponentiates
-//   S(j) and accumulates P(j) V(j), so MFMA and VALU work of one wave overlap;
-//   meanwhile K(j+2) and V(j+1) stream from HBM/L2 into the free stages with
-//   buffer loads that write LDS directly.  One barrier per step hands the
-//   stages over.  The buffer resource's size bound turns rows at or past N
-//   (ragged last block) into zeros.
+// Schedule ("ping-pong", one key block per step)
+//   The two waves of a row group share a SIMD (waves w and w + RG) and run
+//   half a step apart: while one is in its GEMM phase (S(j+1) = K(j+1) Q^T and
+//   O += P(j) V(j), MFMA with fragments from LDS) the other is in its softmax
+//   phase (row max, exponentials, P in bf16, row sums: VALU), so the matrix
+//   core and the VALU of each SIMD are busy at the same time.  A barrier ends
+//   every half step.  LDS holds two K stages and two V stages (slab layout,
+//   see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
+//   step j-1 with buffer loads that write LDS directly, issued during the
+//   first half of step j and waited for at its end.  The buffer resource's
+//   size bound turns rows at or past N (ragged last block) into zeros.
+//   Row sums are plain fp32 additions: a v_dot2 in one wave stalls the MFMAs
+//   of the other wave on the SIMD (measured on gfx950), an add does not.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
@@ -122,8 +127,8 @@ struct Tile {
 // part of the global byte offset.  Rows at or past N fall outside the buffer
 // resource and read as zeros.  The loads are issued from inline assembly so
 // the compiler does not track them: they are waited for explicitly (vmcnt(0)
-// plus a barrier) one pipeline step later, and no compiler-inserted wait can
-// stall the step in between.
+// plus a barrier) at the end of the step, and no compiler-inserted wait can
+// stall the phases in between.
 // One wave load of a tile into LDS bytes 1024*I ..: `rsrc` starts at the
 // tile's first row, `voff` = per-lane offset + the load's uniform offset.
 // The nop is the wait state gfx9 needs between an SALU write of M0 and an
@@ -191,10 +196,9 @@ __device__ __forceinline__ void issue_tile(uint32_t lds, __amdgpu_buffer_rsrc_t 
 }
 
 // The loads of one pipeline step: the next K tile and the next V tile, spread
-// over the step's compute so the wave never stalls on issuing them.  Issued
-// unconditionally so the compute region stays one basic block: near the end
-// of a row the key-block indices repeat the last block and the loads land in
-// slots no later step reads.
+// over the first phase of the step so the wave never stalls on issuing them.
+// Issued unconditionally: near the end of a row the key-block indices repeat
+// the last block and the loads land in slots no later step reads.
 template <int BLOCK>
 struct StepLoads {
   uint32_t k_dst, v_dst;                 // LDS tile addresses
@@ -295,14 +299,17 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int kh, int lane,
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
   if (valid < BLOCK) {
+    // key = lane part + constant part; compare the constant part with a
+    // per-lane limit so no per-element key index is kept in a register.
+    const int lim = valid - (TL::KH * kh + 4 * hl);
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = TL::KH * kh + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
-          if (key >= valid) sc.s[qt][kt][r] = -__builtin_inff();
+          const int off = 32 * kt + 8 * (r / 4) + (r % 4);
+          if (off >= lim) sc.s[qt][kt][r] = -__builtin_inff();
         }
   }
 }
@@ -343,167 +350,114 @@ __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int kh, int lane,
 template <int BLOCK>
 struct Probs {
   bf16x8 p[QT][Tile<BLOCK>::KTW][2];   // [q tile][key tile][k-step half]
-  float alpha[QT];
-  float psum[QT];
-  bool raise;
 };
 
-// Rescale of O when a running max was raised, then O^T += V^T P^T (V tile at
-// lds_v).  k-step (kt, c) holds keys 32kt + 16c + {4h..4h+3, 8+4h..8+4h+3},
-// the keys of C registers 8c..8c+7 of S^T tile kt.  Emitted as one chunk per
-// V fragment with the transposing reads issued two fragments ahead, so the
-// LDS latency hides under the MFMAs of the previous fragments.
+// Softmax phase of the ping-pong schedule: block j's scores (in `sc`) become
+// its probabilities P (bf16, in `pr`), with the running max, the row sums and,
+// when the max is raised, the rescale of O and l done here so that the next
+// GEMM phase only multiplies.  `sl` (may be null) carries tile loads to issue
+// along the way.
 template <int BLOCK>
-__device__ __forceinline__ void accumulate_pv(const Probs<BLOCK>& pr,
-                                              const char* lds_v,
-                                              WaveState<BLOCK>& st,
-                                              const FragAddr& fa) {
+__device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState<BLOCK>& st,
+                                              Probs<BLOCK>& pr, float scale_log2,
+                                              const StepLoads<BLOCK>* sl) {
   using TL = Tile<BLOCK>;
-  // The test also reads the row sums (never negative, so it does not change
-  // the outcome): this keeps the exponentials ahead of the branch, in the
-  // block where they overlap the next block's score MFMAs.
-  float psum_all = 0.f;
+  constexpr int NE = 16 * TL::KTW;   // scores per lane per q tile
+  constexpr int NLOADS = 2 * TL::LOADS;
+  constexpr int LOAD_EVERY = NE / NLOADS >= 2 ? NE / NLOADS : 2;   // scores per load
+  int issued = 0;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) psum_all += pr.psum[qt];
-  if (__builtin_amdgcn_ballot_w64(pr.raise || !(psum_all >= 0.f))) {
+  for (int t = 0; t < QT; ++t) {
+    float mx = -__builtin_inff();
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      st.l[qt] *= pr.alpha[qt];
+    for (int e = 0; e < NE; ++e) mx = fmaxf(mx, sc.s[t][e / 16][e % 16]);
+    const float m = pair_max(mx) * scale_log2;
+    const bool raise = m > st.m[t] + RESCALE_SLACK;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float a = raise ? __builtin_amdgcn_exp2f(st.m[t] - m) : 1.f;
+      st.m[t] = raise ? m : st.m[t];
+      st.l[t] *= a;
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) st.o[qt][dt] *= pr.alpha[qt];
+      for (int dt = 0; dt < 4; ++dt) st.o[t][dt] *= a;
     }
-  }
+    const float msub = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
+    float psv[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) st.l[qt] += pr.psum[qt];
+    for (int el = 0; el < NE; el += 2) {
+      if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
+      const float a = __builtin_amdgcn_exp2f(
+          __builtin_fmaf(sc.s[t][el / 16][el % 16], scale_log2, -msub));
+      const float b = __builtin_amdgcn_exp2f(
+          __builtin_fmaf(sc.s[t][(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
+      const bf16x2 pk = {(__bf16)a, (__bf16)b};
+      psv[(el / 2) % 4] += a + b;
+      pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
+      pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
+    }
+    st.l[t] += (psv[0] + psv[1]) + (psv[2] + psv[3]);
+  }
+  if (sl)
+    for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
+}
 
-  constexpr int FRAGS = 8 * TL::KTW;   // (kt, c, dt)
-  constexpr int AHEAD = 2;
+// GEMM phase of the ping-pong schedule: S(j+1) = K(j+1) Q^T into `sc` and
+// O += P(j) V(j), one MFMA of each in turn (independent accumulators back to
+// back), with K and V fragments read AHEAD MFMAs early and the tile loads in
+// `sl` (may be null) spread over the phase.
+template <int BLOCK>
+__device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
+                                           const bf16x8 (&qf)[QT][8], Scores<BLOCK>& sc,
+                                           const Probs<BLOCK>& pr, WaveState<BLOCK>& st,
+                                           const FragAddr& fa, const StepLoads<BLOCK>* sl) {
+  using TL = Tile<BLOCK>;
+  constexpr int NS = 8 * TL::KTW;   // S MFMAs (per q tile): (key tile, d-step)
+  constexpr int NP = 8 * TL::KTW;   // PV fragments: (key tile, k-step half, d tile)
+  static_assert(NS == NP, "interleave");
+  constexpr int AHEAD = 3;
+  constexpr int NLOADS = 2 * TL::LOADS;
+  auto kfrag = [&](int i) {
+    const int kt = i / 8, stp = i % 8;
+    const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) + (stp / 2) * TL::SLAB +
+                         kt * 32 * SLAB_ROW;
+    return *(const bf16x8*)(lds_k + off);
+  };
   auto vfrag = [&](int f) {
     const int kt = f / 8, c = (f / 4) % 2, dt = f % 4;
     const uint32_t off = dt * TL::SLAB + (32 * kt + 16 * c) * SLAB_ROW;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(lds_v + fa.v_lo + off));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(lds_v + fa.v_hi + off));
-    return __builtin_bit_cast(
-        bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_lo + off));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_hi + off));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  bf16x8 vf[FRAGS];
+  bf16x8 kf[NS], vf[NP];
 #pragma unroll
-  for (int f = 0; f < AHEAD; ++f) vf[f] = vfrag(f);
+  for (int i = 0; i < AHEAD; ++i) {
+    kf[i] = kfrag(i);
+    vf[i] = vfrag(i);
+  }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int f = 0; f < FRAGS; ++f) {
-    if (f + AHEAD < FRAGS) vf[f + AHEAD] = vfrag(f + AHEAD);
-    const int kt = f / 8, c = (f / 4) % 2, dt = f % 4;
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
-      st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          vf[f], pr.p[qt][kt][c], st.o[qt][dt], 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
-// S(j+1) = K(j+1) Q^T fused with block j's softmax arithmetic.  The MFMAs
-// of the next block do not depend on the softmax of the current one, so the
-// region is emitted as one chunk per MFMA, each carrying a slice of the VALU
-// work, with scheduling barriers between chunks so the compiler keeps the
-// interleave: MFMAs of one wave then run under its own exponentials.
-//   chunks 0..7   row-max slices (4 scores of each q tile per chunk)
-//   chunk  8      row statistics: pair max, raise test, alpha, new max
-//   chunks 8..31  exponentials, row sums and bf16 packing of P (64 scores)
-// K fragments are read two MFMA pairs ahead of their use.
-template <int BLOCK>
-__device__ __forceinline__ void scores_with_softmax(
-    const char* lds_k, const bf16x8 (&qf)[QT][8], Scores<BLOCK>& nxt,
-    const Scores<BLOCK>& cur, WaveState<BLOCK>& st, Probs<BLOCK>& pr,
-    const FragAddr& fa, float scale_log2, const StepLoads<BLOCK>& sl) {
-  using TL = Tile<BLOCK>;
-  constexpr int PAIRS = 8 * TL::KTW;      // (key tile, d-step) K fragments
-  constexpr int CHUNKS = QT * PAIRS;      // one MFMA per chunk
-  constexpr int NE = 16 * TL::KTW;        // scores per lane per q tile
-  constexpr int MAX_CHUNKS = CHUNKS / 4;
-  constexpr int EXP_CHUNKS = CHUNKS - MAX_CHUNKS;
-  static_assert(NE % MAX_CHUNKS == 0, "max slices");
-
-  auto kfrag = [&](int pair) {
-    const int kt = pair / 8, stp = pair % 8;
-    const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) +
-                         (stp / 2) * TL::SLAB + kt * 32 * SLAB_ROW;
-    return *(const bf16x8*)(lds_k + off);
-  };
-  auto score = [&](int qt, int e) -> float {   // e: 16*kt + r
-    return cur.s[qt][e / 16][e % 16];
-  };
-  constexpr int AHEAD = 2;                 // K fragments read ahead of use
-
-  bf16x8 kf[PAIRS];
-#pragma unroll
-  for (int i = 0; i < AHEAD; ++i) kf[i] = kfrag(i);
-  float mx[QT], msub[QT], ps[QT];
-#pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    mx[t] = -__builtin_inff();
-    msub[t] = 0.f;
-    ps[t] = 0.f;
-  }
-  bool any_raise = false;
-  constexpr int NLOADS = 2 * TL::LOADS;
-  static_assert(CHUNKS % NLOADS == 0, "load spacing");
-#pragma unroll
-  for (int ch = 0; ch < CHUNKS; ++ch) {
-    const int pair = ch / QT, qt = ch % QT;
-    if (ch % (CHUNKS / NLOADS) == 0) issue_step_load<BLOCK>(sl, ch / (CHUNKS / NLOADS));
-    if (qt == 0 && pair + AHEAD < PAIRS) kf[pair + AHEAD] = kfrag(pair + AHEAD);
+  for (int i = 0; i < NS; ++i) {
+    if (i + AHEAD < NS) {
+      kf[i + AHEAD] = kfrag(i + AHEAD);
+      vf[i + AHEAD] = vfrag(i + AHEAD);
+    }
+    if (sl && i % (NS / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NS / NLOADS));
     {
-      const int kt = pair / 8, stp = pair % 8;
-      nxt.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          kf[pair], qf[qt][stp], stp == 0 ? f32x16{} : nxt.s[qt][kt], 0, 0, 0);
+      const int kt = i / 8, stp = i % 8;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+        sc.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            kf[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
     }
-    if (ch < MAX_CHUNKS) {
-      constexpr int W = NE / MAX_CHUNKS;
+    {
+      const int kt = i / 8, c = (i / 4) % 2, dt = i % 4;
 #pragma unroll
-      for (int t = 0; t < QT; ++t)
-#pragma unroll
-        for (int i = 0; i < W; ++i) mx[t] = fmaxf(mx[t], score(t, ch * W + i));
-    }
-    if (ch == MAX_CHUNKS) {
-#pragma unroll
-      for (int t = 0; t < QT; ++t) {
-        const float m = pair_max(mx[t]) * scale_log2;
-        const bool raise = m > st.m[t] + RESCALE_SLACK;
-        const float a = __builtin_amdgcn_exp2f(st.m[t] - m);
-        pr.alpha[t] = raise ? a : 1.f;
-        st.m[t] = raise ? m : st.m[t];
-        any_raise |= raise;
-        msub[t] = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
-      }
-    }
-    if (ch >= MAX_CHUNKS) {
-      // P in pairs: exponentials, bf16 packing, and the row sum of the
-      // packed values with one dot2 per pair (the sum matches what P.V sees).
-      constexpr int NP = QT * NE / 2;
-      const int p0 = (ch - MAX_CHUNKS) * NP / EXP_CHUNKS;
-      const int p1 = (ch - MAX_CHUNKS + 1) * NP / EXP_CHUNKS;
-#pragma unroll
-      for (int pi = p0; pi < p1; ++pi) {
-        const int t = (2 * pi) / NE, el = (2 * pi) % NE;   // q tile, score index
-        const float a = __builtin_amdgcn_exp2f(
-            __builtin_fmaf(score(t, el), scale_log2, -msub[t]));
-        const float b = __builtin_amdgcn_exp2f(
-            __builtin_fmaf(score(t, el + 1), scale_log2, -msub[t]));
-        const bf16x2 pk = {(__bf16)a, (__bf16)b};
-        ps[t] = __builtin_amdgcn_fdot2_f32_bf16(pk, bf16x2{(__bf16)1.f, (__bf16)1.f},
-                                                ps[t], false);
-        pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
-        pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
-      }
+      for (int qt = 0; qt < QT; ++qt)
+        st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pr.p[qt][kt][c],
+                                                               st.o[qt][dt], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-#pragma unroll
-  for (int t = 0; t < QT; ++t) pr.psum[t] = ps[t];
-  pr.raise = any_raise;
 }
 
 // MODE: ATTN_DENSE (every key block), ATTN_BLOCK (kept blocks of a block
@@ -519,8 +473,8 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   using TL = Tile<BLOCK>;
   constexpr bool SPARSE = MODE != ATTN_DENSE;
   constexpr bool EXACT = MODE == ATTN_EXACT;
-  // Stages: K slots 0-1, V slots 0-2.
-  __shared__ __attribute__((aligned(1024))) char lds[5 * TL::BYTES];
+  // Stages: K slots 0-1, V slots 0-1.
+  __shared__ __attribute__((aligned(1024))) char lds[4 * TL::BYTES];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
 
   const int tid = threadIdx.x;
@@ -616,46 +570,55 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const char* const k_lds = lds;
     const char* const v_lds = lds + 2 * TL::BYTES;
 
-    // Prologue: K(0), V(0) resident, S(0) computed, K(1) resident.
+    // Ping-pong schedule.  The waves of key half 0 ("leaders") run half a
+    // step ahead of those of key half 1, so on each SIMD one wave is in its
+    // GEMM phase (S(j+1) = K(j+1) Q^T and O += P(j) V(j), MFMA) while the
+    // other is in its softmax phase (VALU): half-period 2j is the leaders'
+    // GEMM j and the others' softmax j, half-period 2j+1 the leaders' softmax
+    // j+1 and the others' GEMM j.  A barrier ends every half-period.  K(j+1)
+    // and V(j) stay resident through half-periods 2j and 2j+1; K(j+2) and
+    // V(j+1) are issued in half-period 2j (into the slots of K(j) and V(j-1),
+    // free since half-period 2j-1) and waited for at the end of 2j+1.
+    const bool lead = kh == 0;
     int kb0 = kb_at(0);
     int kb1 = n > 1 ? kb_at(1) : kb0;          // block j+1
     int kb2 = n > 2 ? kb_at(2) : kb1;          // block j+2
     issue_tile<BLOCK>(k_slot0, rk_at(kb0), kp);
     issue_tile<BLOCK>(v_slot0, rv_at(kb0), vp);
+    issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(kb1), kp);
     wait_loads_and_sync();
-    if (n > 1) issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(kb1), kp);
-    Scores<BLOCK> sa, sb;
-    compute_scores<BLOCK>(k_lds, qf, sa, fa);
-    mask_block(sa, kb0);
-    wait_loads_and_sync();
-
+    Scores<BLOCK> sc;
+    compute_scores<BLOCK>(k_lds, qf, sc, fa);   // S(0)
+    mask_block(sc, kb0);
     Probs<BLOCK> pr;
-    int kslot = 1;   // slot of K(j+1)
-    int vslot = 0;   // slot of V(j)
-    // Step j: S(j) is in `cur`; K(j+1), V(j) (and V(j-1)) are resident.
-    // Load K(j+2) and V(j+1) into the slots step j-1 released, compute S(j+1)
-    // into `nxt`, finish block j.
-    auto step = [&](int j, Scores<BLOCK>& cur, Scores<BLOCK>& nxt) {
-      const int kb3v = kb_fetch(j + 3);          // consumed after the barrier
-      const int vnext = vslot == 2 ? 0 : vslot + 1;
+    if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
+    __syncthreads();
+    for (int j = 0; j < n; ++j) {
+      const int kb3v = kb_fetch(j + 3);
       const StepLoads<BLOCK> sl{
-          (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(1 - kslot) * TL::BYTES),
-          (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)vnext * TL::BYTES),
+          (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
+          (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
           rk_at(kb2), rv_at(kb1), &kp, &vp};
-      scores_with_softmax<BLOCK>(k_lds + kslot * TL::BYTES, qf, nxt, cur, ws, pr,
-                                 fa, scale_log2, sl);
-      accumulate_pv<BLOCK>(pr, v_lds + vslot * TL::BYTES, ws, fa);
-      mask_block(nxt, kb1);
-      kslot = 1 - kslot;
-      vslot = vnext;
+      const char* const kj1 = k_lds + ((j + 1) & 1) * TL::BYTES;   // K(j+1)
+      const char* const vj = v_lds + (j & 1) * TL::BYTES;          // V(j)
+      // half-period 2j
+      if (lead) {
+        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, &sl);
+        mask_block(sc, kb1);
+      } else {
+        softmax_phase<BLOCK>(sc, ws, pr, scale_log2, &sl);
+      }
+      __syncthreads();
+      // half-period 2j+1
+      if (lead) {
+        if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
+      } else {
+        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, nullptr);
+        mask_block(sc, kb1);
+      }
       wait_loads_and_sync();
       kb1 = kb2;
       kb2 = __builtin_amdgcn_readfirstlane(kb3v);
-    };
-    for (int j = 0; j < n; j += 2) {
-      step(j, sa, sb);
-      if (j + 1 >= n) break;
-      step(j + 1, sb, sa);
     }
     __syncthreads();
   }
