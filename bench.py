@@ -356,7 +356,7 @@ def main():
         **({"pattern_variants": variants} if variants else {}),
         **dense,
         "roofline": {
-            "kernel": "attn_fwd_kernel<128, sparse>",
+            "kernel": "attn_fwd_kernel<128, ATTN_BLOCK>",
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

@@ -381,7 +381,7 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
       for (int dt = 0; dt < 4; ++dt) st.o[t][dt] *= a;
     }
     const float msub = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
-    float psv[4] = {0.f, 0.f, 0.f, 0.f};
+    float psv[4];   // four partial row sums (independent add chains)
 #pragma unroll
     for (int el = 0; el < NE; el += 2) {
       if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
@@ -390,7 +390,7 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
       const float b = __builtin_amdgcn_exp2f(
           __builtin_fmaf(sc.s[t][(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
       const bf16x2 pk = {(__bf16)a, (__bf16)b};
-      psv[(el / 2) % 4] += a + b;
+      psv[(el / 2) % 4] = el < 8 ? a + b : psv[(el / 2) % 4] + (a + b);
       pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
       pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
     }
