@@ -175,3 +175,35 @@ def test_strided_layout_matches_contiguous():
     b = L.attention(qn, kn, vn, csr.device_mask(), out=on)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# Degenerate shapes: fewer tokens than one block, a single frame (the mask is
+# then full), two frames with one-block rows, and the smallest frames.
+EDGE = [
+    # T, P, B, H, W, T_per
+    (1, 10, 128, 1, 0, 1),      # N = 10 < B: one ragged block
+    (1, 200, 64, 2, 0, 1),      # T = 1: every query attends its own frame only
+    (2, 40, 128, 1, 0, 2),      # N = 80 < B, two frames in one block
+    (3, 1, 64, 1, 0, 3),        # P = 1: frames of a single token
+    (5, 64, 64, 1, 0, 5),       # one kept block per row besides the anchor's
+]
+
+
+@pytest.mark.parametrize("T,P,B,H,W,tper", EDGE)
+def test_edge_shapes(T, P, B, H, W, tper):
+    _say(f"[edge] T={T} P={P} B={B} H={H} W={W} tper={tper}")
+    N = T * P
+    q, k, v = make_qkv(H, N, seed=N + B)
+    p = L.Params(window=W, tper=tper)
+    csr = L.build_mask(T, P, B, 0, p)
+    csr.upload()
+    out = L.attention(q.cuda(), k.cuda(), v.cuda(), csr.device_mask())
+    torch.cuda.synchronize()
+    rp, ci = M.build_mask(T, P, B, 0, W=W, tper=tper)
+    assert csr.arrays()[0].tolist() == rp and csr.arrays()[1].tolist() == ci
+    ref = OA.assemble(OA.block_sparse_attention(q.float().numpy(), k.float().numpy(),
+                                                v.float().numpy(), rp, ci, B),
+                      H, N, 128, B)
+    err = np.abs(out.float().cpu().numpy() - ref)
+    assert np.isfinite(out.float().cpu().numpy()).all()
+    assert_close(float(err.max()), float(err.mean()))

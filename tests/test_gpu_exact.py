@@ -162,3 +162,19 @@ def test_exact_with_device_built_mask_and_determinism():
     torch.cuda.synchronize()
     assert torch.equal(a, b) and torch.equal(b, c)
     assert MAX_ABS > 0 and MEAN_ABS > 0
+
+
+def test_exact_strided_layout_matches_contiguous():
+    """[N, H, d] storage (token stride H*d) gives the same bits as [H, N, d]
+    for the token-exact form too."""
+    T, P, B, H = 5, 300, 128, 3
+    N = T * P
+    q, k, v = make_qkv(H, N, seed=19)
+    csr = L.build_mask(T, P, B, 2, L.Params(window=1, tper=2), exact=True)
+    csr.upload()
+    a = L.attention_exact(q.cuda(), k.cuda(), v.cuda(), csr.exact_mask())
+    qn, kn, vn = (x.transpose(0, 1).contiguous().cuda().transpose(0, 1) for x in (q, k, v))
+    on = torch.empty((N, H, 128), dtype=torch.bfloat16, device="cuda").transpose(0, 1)
+    b = L.attention_exact(qn, kn, vn, csr.exact_mask(), out=on)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
