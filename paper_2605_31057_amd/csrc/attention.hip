@@ -13,12 +13,12 @@
 //   once at the end.
 //
 // Schedule ("ping-pong", one key block per step)
-//   The two waves of a row group share a SIMD (waves w and w + RG) and run
-//   half a step apart: while one is in its GEMM phase (S(j+1) = K(j+1) Q^T and
-//   O += P(j) V(j), MFMA with fragments from LDS) the other is in its softmax
-//   phase (row max, exponentials, P in bf16, row sums: VALU), so the matrix
-//   core and the VALU of each SIMD are busy at the same time.  A barrier ends
-//   every half step.  LDS holds two K stages and two V stages (slab layout,
+//   The two waves of a row group (waves w and w + RG, which share a SIMD when
+//   the workgroup has 8 waves) run half a step apart: while one is in its
+//   GEMM phase (S(j+1) = K(j+1) Q^T and O += P(j) V(j), MFMA with fragments
+//   from LDS) the other is in its softmax phase (row max, exponentials, P in
+//   bf16, row sums: VALU), so the matrix core and the VALU of each SIMD are
+//   busy at the same time.  A barrier ends every half step.  LDS holds two K stages and two V stages (slab layout,
 //   see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
 //   step j-1 with buffer loads that write LDS directly, issued during the
 //   first half of step j and waited for at its end.  The buffer resource's
@@ -53,7 +53,6 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int D = 128;             // head_dim
-constexpr int ROW_BYTES = D * 2;   // one K/V row in LDS
 constexpr float RESCALE_SLACK = 8.f;
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -565,7 +564,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   }
 
   if (n > 0) {
-    // LDS stages: K(b) in K slot b % 2, V(b) in V slot b % 3.
+    // LDS stages: K(b) in K slot b % 2, V(b) in V slot b % 2.
     const uint32_t k_slot0 = lds_base, v_slot0 = lds_base + 2 * TL::BYTES;
     const char* const k_lds = lds;
     const char* const v_lds = lds + 2 * TL::BYTES;
