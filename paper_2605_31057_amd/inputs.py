@@ -69,6 +69,11 @@ WORKLOADS = {
     "hv15_2x": Workload("hv15_2x", 16, 65, 1590, 128, budget_frames=33, window=6,
                         steps=tuple(range(50)), layers=(0, 1, 2, 3),
                         desc="HunyuanVideo-1.5 layer, 65 x 30x53 tokens, 16 heads"),
+    # The same layer with the Wan budget C = 21 instead of 33 (a labelled
+    # variant: C = 33 leaves 30 of 33 frames at the 1x horizon).
+    "hv15_2x_c21": Workload("hv15_2x_c21", 16, 65, 1590, 128, budget_frames=21, window=6,
+                            steps=(0, 10),
+                            desc="HunyuanVideo-1.5 layer, 65 x 30x53 tokens, 16 heads, C=21"),
     # The same layer with the dual-stream text tokens in self-attention: 512
     # text tokens (prompts of about 500 tokens) after the video tokens.
     "hv15_2x_text": Workload("hv15_2x_text", 16, 65, 1590, 128, budget_frames=33,
