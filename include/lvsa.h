@@ -175,13 +175,16 @@ typedef struct lvsa_block_mask {
 /* Errors: EINVAL if the handle was never uploaded. */
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
 
-/* Device builder: the same mask computed by one kernel on `stream`, written
- * to caller-owned device buffers (no host round trip, no allocation).
+/* Device builder: the same mask computed on the GPU (three short kernels on
+ * `stream`), written to caller-owned device buffers (no host round trip, no
+ * allocation).
  *   d_row_ptr    device int32[nb + 1]
  *   d_col_idx    device int32[col_capacity]; col_capacity must be at least
  *                nb * nb (the mask's worst case), so every write is in bounds
  * Arguments as for lvsa_build_mask; T <= LVSA_MAX_FRAMES.
- * Errors: EINVAL (ranges, nulls, capacity), EDEVICE (launch). */
+ * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED when a block would
+ * touch more than 1024 frames (B/P + 2 > 1024 and T > 1024), EDEVICE
+ * (launch). */
 lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t step, int32_t layer,
                                    const lvsa_params* p, int32_t* d_row_ptr,

@@ -289,6 +289,7 @@ lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
   if (st != LVSA_OK) return st;
   const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (!exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
+  if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
   if (entry_capacity < nb * nb) return LVSA_EINVAL;
   if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry,
                                (hipStream_t)stream) != hipSuccess)
@@ -308,6 +309,7 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
   st = check_mask_shape(T, P, B, c.text);
   if (st != LVSA_OK) return st;
   const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
+  if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
   if (col_capacity < nb * nb) return LVSA_EINVAL;
   if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr,
                                (hipStream_t)stream) != hipSuccess)

@@ -33,7 +33,10 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<uint32_t>* entry);
 
 // Device CSR construction (mask_device.hip).  Writes row_ptr and, where the
-// pointer is non-null, col_idx and/or the token-exact entry words.
+// pointer is non-null, col_idx and/or the token-exact entry words.  The
+// builder holds the windows of one query block's frames in LDS:
+// device_mask_supported says whether a block touches few enough frames.
+bool device_mask_supported(const FrameCfg& c, int32_t P, int32_t B);
 hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
                                     uint32_t* d_entry, hipStream_t stream);
