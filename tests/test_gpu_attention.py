@@ -207,3 +207,31 @@ def test_edge_shapes(T, P, B, H, W, tper):
     err = np.abs(out.float().cpu().numpy() - ref)
     assert np.isfinite(out.float().cpu().numpy()).all()
     assert_close(float(err.max()), float(err.mean()))
+
+
+@pytest.mark.parametrize("scale", [8.0, 30.0])
+def test_large_logits_exercise_the_rescale(scale):
+    """Q and K scaled up so logits span hundreds of log2 units: the running
+    max is raised on most key blocks (the rescale of O and l runs often) and
+    the result still matches the fp32 oracle."""
+    T, P, B, H = 6, 200, 128, 2
+    N = T * P
+    _say(f"[large-logits] scale {scale}")
+    q, k, v = make_qkv(H, N, seed=int(scale))
+    q = (q.float() * scale).to(torch.bfloat16)
+    k = (k.float() * scale).to(torch.bfloat16)
+    csr = L.build_mask(T, P, B, 1, L.Params(window=1, tper=3))
+    csr.upload()
+    out = L.attention(q.cuda(), k.cuda(), v.cuda(), csr.device_mask())
+    dense = L.dense_attention(q.cuda(), k.cuda(), v.cuda(), block=B)
+    torch.cuda.synchronize()
+    rp, ci = M.build_mask(T, P, B, 1, W=1, tper=3)
+    qf, kf, vf = (x.float().numpy() for x in (q, k, v))
+    ref = OA.assemble(OA.block_sparse_attention(qf, kf, vf, rp, ci, B), H, N, 128, B)
+    g = out.float().cpu().numpy()
+    assert np.isfinite(g).all()
+    err = np.abs(g - ref)
+    assert_close(float(err.max()), float(err.mean()))
+    dref = OA.dense_attention(qf, kf, vf)
+    err = np.abs(dense.float().cpu().numpy() - dref)
+    assert_close(float(err.max()), float(err.mean()))
