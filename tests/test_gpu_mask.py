@@ -135,3 +135,27 @@ def test_pattern_variant_attention_parity(mode, rotate, extra):
         fref = OA.frame_sparse_attention(qf, kf, vf, A, P)
         err = np.abs(ex.float().cpu().numpy() - fref)
         assert_close(float(err.max()), float(err.mean()))
+
+
+def test_pattern_variants_full_size_sampled_rows():
+    """The five pattern variants the bench times, at the full Wan-1.3B 6x
+    shape in one launch each, checked on sampled query blocks of two heads."""
+    from paper_2605_31057_amd.inputs import WORKLOADS, workload_qkv
+    from tests.gpu_util import compare_rows, sample_q_blocks
+    w = WORKLOADS["wan13_6x"]
+    print("[pattern-full] generating inputs", flush=True)
+    q, k, v = workload_qkv(w, heads=2)
+    qd, kd, vd = (x.cuda() for x in (q, k, v))
+    for mode, rotate, extra in [(L.WINDOW_EXPANDED, 1, 0), (L.WINDOW_ADAPTIVE, 1, 0),
+                                (L.WINDOW_BASIC, 1, 0), (L.WINDOW_EXPANDED, 0, 0),
+                                (L.WINDOW_EXPANDED, 1, 1)]:
+        print(f"[pattern-full] mode {mode} rotate {rotate} extra {extra}", flush=True)
+        p = L.Params(window_mode=mode, rotate=rotate, extra_anchors=extra)
+        csr = L.build_mask(w.frames, w.tokens_per_frame, w.block, 10, p)
+        csr.upload()
+        out = L.attention(qd, kd, vd, csr.device_mask())
+        torch.cuda.synchronize()
+        rp, ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, 10, **_kw(p))
+        assert csr.arrays()[0].tolist() == rp
+        qbs = sample_q_blocks(rp, w.frames, w.tokens_per_frame, w.block, n_random=1)
+        assert_close(*compare_rows(out, q, k, v, rp, ci, w.block, [0, 1], qbs))
