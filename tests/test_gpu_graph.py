@@ -67,3 +67,42 @@ def test_step_in_hip_graph_replays_match_eager():
         assert torch.equal(got, out), f"replay {rep}: block form differs from eager"
         assert torch.equal(got_x, out_x), f"replay {rep}: exact form differs from eager"
         assert bool(torch.isfinite(got.float()).all())
+
+
+def test_concurrent_streams_are_independent():
+    """Two steps with different masks and inputs in flight on two streams at
+    once give the bits each gives alone (the library keeps no global state)."""
+    T, P, B, H = 8, 300, 128, 2
+    N = T * P
+    nb = -(-N // B)
+    print("[streams] two concurrent steps", flush=True)
+    ins = [tuple(x.cuda() for x in make_qkv(H, N, seed=s)) for s in (51, 52)]
+    params = [L.Params(window=1, tper=3), L.Params(window=0, tper=2, window_mode=L.WINDOW_BASIC)]
+    bufs = [(torch.empty(nb + 1, dtype=torch.int32, device="cuda"),
+             torch.empty(nb * nb, dtype=torch.int32, device="cuda")) for _ in range(2)]
+    outs = [torch.empty_like(ins[0][0]) for _ in range(2)]
+
+    def step(i, stream):
+        rp, ci = bufs[i]
+        m = L.build_mask_device(T, P, B, 3 + i, rp, ci, params=params[i], stream=stream)
+        q, k, v = ins[i]
+        L.attention(q, k, v, m, out=outs[i], stream=stream)
+
+    alone = []
+    for i in range(2):
+        step(i, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        alone.append(outs[i].clone())
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for _ in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        for s in streams:
+            s.wait_stream(torch.cuda.current_stream())
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                step(i, streams[i])
+        torch.cuda.synchronize()
+        for i in range(2):
+            assert torch.equal(outs[i], alone[i]), i
