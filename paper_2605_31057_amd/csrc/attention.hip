@@ -17,14 +17,17 @@
 //   the workgroup has 8 waves) run half a step apart: while one is in its
 //   GEMM phase (S(j+1) = K(j+1) Q^T and O += P(j) V(j), MFMA with fragments
 //   from LDS) the other is in its softmax phase (row max, exponentials, P in
-//   bf16, row sums: VALU), so the matrix core and the VALU of each SIMD are
-//   busy at the same time.  A barrier ends every half step.  LDS holds two K stages and two V stages (slab layout,
-//   see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
+//   bf16: VALU), so the matrix core and the VALU of each SIMD are busy at the
+//   same time.  A barrier ends every half step.  LDS holds two K stages and
+//   two V stages (slab layout, see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
 //   step j-1 with buffer loads that write LDS directly, issued during the
 //   first half of step j and waited for at its end.  The buffer resource's
 //   size bound turns rows at or past N (ragged last block) into zeros.
-//   Row sums are plain fp32 additions: a v_dot2 in one wave stalls the MFMAs
-//   of the other wave on the SIMD (measured on gfx950), an add does not.
+//   Row sums come from the matrix core: in the GEMM phase a 16x16x32 MFMA
+//   with a constant 0/1 A operand adds up each 16-key step of P for all 32
+//   rows of the wave.  That takes 32 adds per step off the softmax phase, whose
+//   wave issues its VALU work alone on the SIMD, for 4 small MFMAs (1/16 of
+//   the step's matrix work), and sums exactly the bf16 P that multiplies V.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
@@ -51,6 +54,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int D = 128;             // head_dim
 constexpr float RESCALE_SLACK = 8.f;
@@ -78,11 +82,6 @@ __device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
                                             __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair_sum(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
-                                            __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // LDS tile layout ("slabs").  A BLOCK x 128 tile is stored as 4 slabs of 32
@@ -287,7 +286,7 @@ template <int BLOCK>
 struct WaveState {
   f32x16 o[QT][4];   // O^T tiles [q tile][d tile]: d = 32*dt + C row
   float m[QT];       // running max (log2 domain), shared by lanes l, l^32
-  float l[QT];       // partial row sums of this lane's keys
+  f32x4 l[QT];       // row sums (MFMA 16x16 C tile: lane c < 16 holds rows c, c + 16)
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
@@ -352,9 +351,9 @@ struct Probs {
 };
 
 // Softmax phase of the ping-pong schedule: block j's scores (in `sc`) become
-// its probabilities P (bf16, in `pr`), with the running max, the row sums and,
-// when the max is raised, the rescale of O and l done here so that the next
-// GEMM phase only multiplies.  `sl` (may be null) carries tile loads to issue
+// its probabilities P (bf16, in `pr`), with the running max and, when the
+// max is raised, the rescale of O and l done here so that the next GEMM phase
+// only multiplies (and adds P up into l).  `sl` (may be null) carries tile loads to issue
 // along the way.
 template <int BLOCK>
 __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState<BLOCK>& st,
@@ -375,12 +374,14 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
     if (__builtin_amdgcn_ballot_w64(raise)) {
       const float a = raise ? __builtin_amdgcn_exp2f(st.m[t] - m) : 1.f;
       st.m[t] = raise ? m : st.m[t];
-      st.l[t] *= a;
+      // l tile: register 0 of lane c holds row c, register 1 row c + 16.
+      const float a16 = __shfl_xor(a, 16);
+      st.l[t][0] *= a;
+      st.l[t][1] *= a16;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) st.o[t][dt] *= a;
     }
     const float msub = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
-    float psv[4];   // four partial row sums (independent add chains)
 #pragma unroll
     for (int el = 0; el < NE; el += 2) {
       if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
@@ -389,11 +390,9 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
       const float b = __builtin_amdgcn_exp2f(
           __builtin_fmaf(sc.s[t][(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
       const bf16x2 pk = {(__bf16)a, (__bf16)b};
-      psv[(el / 2) % 4] = el < 8 ? a + b : psv[(el / 2) % 4] + (a + b);
       pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
       pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
     }
-    st.l[t] += (psv[0] + psv[1]) + (psv[2] + psv[3]);
   }
   if (sl)
     for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
@@ -401,13 +400,15 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
 
 // GEMM phase of the ping-pong schedule: S(j+1) = K(j+1) Q^T into `sc` and
 // O += P(j) V(j), one MFMA of each in turn (independent accumulators back to
-// back), with K and V fragments read AHEAD MFMAs early and the tile loads in
-// `sl` (may be null) spread over the phase.
+// back), l += the row sums of P(j) (one 16x16x32 MFMA per 16-key step, `ones`
+// its A operand), with K and V fragments read AHEAD MFMAs early and the tile
+// loads in `sl` (may be null) spread over the phase.
 template <int BLOCK>
 __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
                                            const bf16x8 (&qf)[QT][8], Scores<BLOCK>& sc,
                                            const Probs<BLOCK>& pr, WaveState<BLOCK>& st,
-                                           const FragAddr& fa, const StepLoads<BLOCK>* sl) {
+                                           const FragAddr& fa, const bf16x8& ones,
+                                           const StepLoads<BLOCK>* sl) {
   using TL = Tile<BLOCK>;
   constexpr int NS = 8 * TL::KTW;   // S MFMAs (per q tile): (key tile, d-step)
   constexpr int NP = 8 * TL::KTW;   // PV fragments: (key tile, k-step half, d tile)
@@ -454,6 +455,11 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
       for (int qt = 0; qt < QT; ++qt)
         st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pr.p[qt][kt][c],
                                                                st.o[qt][dt], 0, 0, 0);
+      if (dt == 3)
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+          st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt][c], st.l[qt],
+                                                             0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -560,7 +566,17 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) ws.o[qt][dt] = f32x16{};
     ws.m[qt] = -__builtin_inff();
-    ws.l[qt] = 0.f;
+    ws.l[qt] = f32x4{};
+  }
+  // A operand of the row-sum MFMA (16x16x32): read as P^T's B operand, lane
+  // group g = lane/16 of the 32x32 P register holds q rows 16*(g%2) + 0..15,
+  // so A row 0 takes groups 0 and 2 (rows 0-15) and row 1 groups 1 and 3.
+  bf16x8 ones;
+  {
+    const int ai = lane % 16, ag = lane / 16;
+    const bool one = (ai == 0 && ag % 2 == 0) || (ai == 1 && ag % 2 == 1);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = one ? (__bf16)1.f : (__bf16)0.f;
   }
 
   if (n > 0) {
@@ -602,7 +618,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       const char* const vj = v_lds + (j & 1) * TL::BYTES;          // V(j)
       // half-period 2j
       if (lead) {
-        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, &sl);
+        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, &sl);
         mask_block(sc, kb1);
       } else {
         softmax_phase<BLOCK>(sc, ws, pr, scale_log2, &sl);
@@ -612,7 +628,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       if (lead) {
         if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
       } else {
-        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, nullptr);
+        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
         mask_block(sc, kb1);
       }
       wait_loads_and_sync();
@@ -630,7 +646,10 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   float* ml = mm + TL::RG * QT * 64;            // [RG][QT][64 lanes] pair sums
   float lsum[QT];
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) lsum[qt] = pair_sum(ws.l[qt]);
+  for (int qt = 0; qt < QT; ++qt) {
+    const float r0 = __shfl(ws.l[qt][0], li), r1 = __shfl(ws.l[qt][1], li & 15);
+    lsum[qt] = li < 16 ? r0 : r1;
+  }
   if (kh == 1) {
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
