@@ -150,46 +150,73 @@ lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
                           int32_t* block, int32_t* n_blocks, int64_t* nnz,
                           const int32_t** row_ptr, const int32_t** col_idx);
 
-/* Copies the host arrays (and the token-exact entry words, when the handle
- * has them) to device memory owned by the handle (allocated on the first
- * call, on the current device), asynchronously on `stream`; the
- * host arrays must stay unmodified until the stream reaches the copy, which
- * lvsa_csr_free respects by synchronizing the device before releasing.
- * Errors: EINVAL (null), ENOMEM, EDEVICE. */
+/* Copies the host arrays, the pair schedule (below) and, when the handle has
+ * them, the token-exact entry words and pair words to device memory owned by
+ * the handle (allocated on the first call, on the current device),
+ * asynchronously on `stream`; the host arrays must stay unmodified until the
+ * stream reaches the copy, which lvsa_csr_free respects by synchronizing the
+ * device before releasing.  Errors: EINVAL (null), ENOMEM, EDEVICE. */
 lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream);
 
 /* Releases host and device memory of the handle.  NULL is accepted. */
 void lvsa_csr_free(lvsa_csr* csr);
 
-/* Device-resident block CSR: what the attention kernel reads.  Fill it from
- * an uploaded handle with lvsa_csr_device_view, or point it at buffers
- * written by lvsa_build_mask_device. */
+/* Pair schedule: the same mask arranged for the attention kernel, which
+ * handles query blocks two at a time.  Row p (p < np = ceil(nb / 2)) lists,
+ * in ascending order and without repeats, the key blocks kept by query
+ * block 2p or by 2p+1 (the union of CSR rows 2p and 2p+1; the last row of an
+ * odd nb has one query block), one 32-bit word each:
+ *   block form   bits  0..29  kb
+ *                bit  30      query block 2p keeps kb
+ *                bit  31      query block 2p+1 keeps kb
+ * (the token-exact form of the words is given with lvsa_exact_mask).
+ * pair_ptr[np + 1] delimits the rows (pair_ptr[0] = 0); a row holds at most
+ * nb words and all rows together at most nnz. */
+
+/* Host arrays of a handle's pair schedule (valid until lvsa_csr_free):
+ * np rows, n_words words, block-form words, and the token-exact words of a
+ * handle built by lvsa_build_exact_mask (NULL otherwise).  Any output pointer
+ * may be NULL.  Errors: EINVAL (null handle). */
+lvsa_status lvsa_csr_pairs(const lvsa_csr* csr, int32_t* n_pairs, int64_t* n_words,
+                           const int32_t** pair_ptr, const uint32_t** pair_word,
+                           const uint32_t** pair_exact);
+
+/* Device-resident block mask: the CSR and its pair schedule, which is what
+ * the attention kernel reads.  Fill it from an uploaded handle with
+ * lvsa_csr_device_view, or point it at buffers written by
+ * lvsa_build_mask_device. */
 typedef struct lvsa_block_mask {
-  int32_t n_tokens;       /* N                                             */
-  int32_t block;          /* B, tokens per query block and per key block  */
-  int32_t n_blocks;       /* nb = ceil(N / B)                              */
-  const int32_t* row_ptr; /* device, [nb + 1], row_ptr[0] = 0, ascending   */
-  const int32_t* col_idx; /* device, [row_ptr[nb]], each row ascending     */
+  int32_t n_tokens;         /* N                                           */
+  int32_t block;            /* B, tokens per query block and per key block */
+  int32_t n_blocks;         /* nb = ceil(N / B)                            */
+  const int32_t* row_ptr;   /* device, [nb + 1], row_ptr[0] = 0, ascending */
+  const int32_t* col_idx;   /* device, [row_ptr[nb]], each row ascending   */
+  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1]                  */
+  const uint32_t* pair_word;/* device, block-form pair words               */
 } lvsa_block_mask;
 
 /* Errors: EINVAL if the handle was never uploaded. */
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
 
-/* Device builder: the same mask computed on the GPU (three short kernels on
- * `stream`), written to caller-owned device buffers (no host round trip, no
- * allocation).
- *   d_row_ptr    device int32[nb + 1]
- *   d_col_idx    device int32[col_capacity]; col_capacity must be at least
- *                nb * nb (the mask's worst case), so every write is in bounds
+/* Device builder: the same mask and its pair schedule computed on the GPU
+ * (six short kernels on `stream`), written to caller-owned device buffers
+ * (no host round trip, no allocation).
+ *   d_row_ptr     device int32[nb + 1]
+ *   d_col_idx     device int32[col_capacity]; col_capacity must be at least
+ *                 nb * nb (the mask's worst case), so every write is in bounds
+ *   d_pair_ptr    device int32[ceil(nb / 2) + 1]
+ *   d_pair_word   device uint32[pair_capacity], pair_capacity at least
+ *                 ceil(nb / 2) * nb; block-form words
  * Arguments as for lvsa_build_mask; T <= LVSA_MAX_FRAMES.
- * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED when a block would
- * touch more than 1024 frames (B/P + 2 > 1024 and T > 1024), EDEVICE
- * (launch). */
+ * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED when a query-block
+ * pair would touch more than 1024 frames (2B/P + 2 > 1024 and T > 1024),
+ * EDEVICE (launch). */
 lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t step, int32_t layer,
                                    const lvsa_params* p, int32_t* d_row_ptr,
                                    int32_t* d_col_idx, int64_t col_capacity,
-                                   void* stream);
+                                   int32_t* d_pair_ptr, uint32_t* d_pair_word,
+                                   int64_t pair_capacity, void* stream);
 
 /* ------------------------------------------------ token-exact form ---- */
 
@@ -211,14 +238,23 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
  *                A(a ? f1 : f0)
  *   bits 28..31  zero
  * Query token i of qb attends key token j of kb iff pattern bit
- * 2*(segment(i) != f0) + (segment(j) != g0) is set. */
+ * 2*(segment(i) != f0) + (segment(j) != g0) is set.
+ *
+ * Token-exact pair words (the pair schedule's rows, as in the block form):
+ *   bits  0..15  kb
+ *   bits 16..23  kfirst
+ *   bits 24..27  pattern of (2p, kb), 0 when 2p does not keep kb
+ *   bits 28..31  pattern of (2p+1, kb), 0 when 2p+1 does not keep kb
+ * (a kept block's pattern is never 0). */
 typedef struct lvsa_exact_mask {
-  int32_t n_tokens;        /* N = T*P                                       */
-  int32_t block;           /* B                                             */
-  int32_t n_blocks;        /* nb = ceil(N / B)                              */
-  int32_t frame_tokens;    /* P >= B                                        */
-  const int32_t* row_ptr;  /* device, [nb + 1], as in lvsa_block_mask       */
-  const uint32_t* entry;   /* device, [row_ptr[nb]] entry words, kb ascending */
+  int32_t n_tokens;         /* N = T*P                                      */
+  int32_t block;            /* B                                            */
+  int32_t n_blocks;         /* nb = ceil(N / B)                             */
+  int32_t frame_tokens;     /* P >= B                                       */
+  const int32_t* row_ptr;   /* device, [nb + 1], as in lvsa_block_mask      */
+  const uint32_t* entry;    /* device, [row_ptr[nb]] entry words, kb ascending */
+  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1]                   */
+  const uint32_t* pair_word;/* device, token-exact pair words               */
 } lvsa_exact_mask;
 
 /* Host builder of the token-exact form: the handle of lvsa_build_mask
@@ -236,21 +272,28 @@ lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
                              const uint32_t** entry);
 
 /* Device view of the token-exact form of an uploaded handle built by
- * lvsa_build_exact_mask (lvsa_csr_upload copies the entry words too).
+ * lvsa_build_exact_mask (lvsa_csr_upload copies the entry words and the
+ * token-exact pair words too).
  * Errors: EINVAL if never uploaded, EUNSUPPORTED as for lvsa_csr_entries. */
 lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out);
 
-/* Device builder of the token-exact form: row_ptr and entry words of the
- * same mask as lvsa_build_mask_device, on `stream`, into caller-owned buffers
- *   d_row_ptr  device int32[nb + 1]
- *   d_entry    device uint32[entry_capacity], entry_capacity >= nb * nb
+/* Device builder of the token-exact form: row_ptr, entry words and the
+ * token-exact pair schedule of the same mask as lvsa_build_mask_device, on
+ * `stream`, into caller-owned buffers
+ *   d_row_ptr    device int32[nb + 1]
+ *   d_entry      device uint32[entry_capacity], entry_capacity >= nb * nb
+ *   d_pair_ptr   device int32[ceil(nb / 2) + 1]
+ *   d_pair_word  device uint32[pair_capacity], pair_capacity >=
+ *                ceil(nb / 2) * nb; token-exact pair words
  * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED (P < B, B > 255,
- * nb > 65536), EDEVICE (launch). */
+ * nb > 65536, or as for lvsa_build_mask_device), EDEVICE (launch). */
 lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
                                          int32_t step, int32_t layer,
                                          const lvsa_params* p,
                                          int32_t* d_row_ptr, uint32_t* d_entry,
-                                         int64_t entry_capacity, void* stream);
+                                         int64_t entry_capacity, int32_t* d_pair_ptr,
+                                         uint32_t* d_pair_word, int64_t pair_capacity,
+                                         void* stream);
 
 /* --------------------------------------------------------- attention ---- */
 
@@ -267,7 +310,8 @@ typedef struct lvsa_tensor {
   int64_t stride_token;
 } lvsa_tensor;
 
-/* Block-sparse attention forward (Eq. 2 over the kept blocks of `mask`):
+/* Block-sparse attention forward (Eq. 2 over the kept blocks of `mask`, read
+ * from its pair schedule):
  *   out[h, i] = sum_j softmax_j(q[h,i] . k[h,j] / sqrt(d)) v[h,j]
  * with j over the real tokens (j < N) of the key blocks kept for the query
  * block of i.  bf16 inputs, fp32 products and softmax, bf16 output (round to
@@ -275,15 +319,15 @@ typedef struct lvsa_tensor {
  * head_dim = 128; mask->block is 64 or 128.  Rows i >= N of `out` are never
  * written.  out must not overlap q, k or v.  The result is deterministic
  * (fixed key order per row).
- * Errors: EINVAL (nulls, shape mismatch), EUNSUPPORTED (head_dim, block,
- * alignment), EDEVICE (launch). */
+ * Errors: EINVAL (nulls, including the pair schedule, shape mismatch),
+ * EUNSUPPORTED (head_dim, block, alignment), EDEVICE (launch). */
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream);
 
 /* Token-exact attention forward (Eq. 2 token for token): as lvsa_attention,
  * with the keys of each kept block further restricted, per query token, by
- * the block's entry word, so query i attends exactly the keys j with
+ * the block's pattern (from the token-exact pair words), so query i attends exactly the keys j with
  * frame(j) in A(frame(i)).  mask->block is 64 or 128 and mask->frame_tokens
  * >= mask->block; every query token keeps at least its own frame's keys.
  * Errors as for lvsa_attention. */

@@ -62,15 +62,17 @@ class Params(ctypes.Structure):
 
 
 class BlockMask(ctypes.Structure):
-    """lvsa_block_mask: device-resident block CSR view."""
+    """lvsa_block_mask: device-resident block CSR and its pair schedule."""
     _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_blocks", _i32),
-                ("row_ptr", _p), ("col_idx", _p)]
+                ("row_ptr", _p), ("col_idx", _p), ("pair_ptr", _p), ("pair_word", _p)]
 
 
 class ExactMask(ctypes.Structure):
-    """lvsa_exact_mask: device-resident token-exact form (row_ptr + entry words)."""
+    """lvsa_exact_mask: device-resident token-exact form (row_ptr, entry
+    words and the token-exact pair schedule)."""
     _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_blocks", _i32),
-                ("frame_tokens", _i32), ("row_ptr", _p), ("entry", _p)]
+                ("frame_tokens", _i32), ("row_ptr", _p), ("entry", _p),
+                ("pair_ptr", _p), ("pair_word", _p)]
 
 
 class _Tensor(ctypes.Structure):
@@ -107,7 +109,11 @@ def lib():
             "lvsa_csr_device_view": (_i32, [_p, ctypes.POINTER(BlockMask)]),
             "lvsa_build_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                               ctypes.POINTER(Params), _p, _p,
-                                              _i64, _p]),
+                                              _i64, _p, _p, _i64, _p]),
+            "lvsa_csr_pairs": (_i32, [_p, _pi32, ctypes.POINTER(_i64),
+                                      ctypes.POINTER(_pi32),
+                                      ctypes.POINTER(ctypes.POINTER(ctypes.c_uint32)),
+                                      ctypes.POINTER(ctypes.POINTER(ctypes.c_uint32))]),
             "lvsa_build_exact_mask": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                              ctypes.POINTER(Params),
                                              ctypes.POINTER(_p)]),
@@ -116,7 +122,7 @@ def lib():
             "lvsa_csr_exact_view": (_i32, [_p, ctypes.POINTER(ExactMask)]),
             "lvsa_build_exact_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                                     ctypes.POINTER(Params), _p, _p,
-                                                    _i64, _p]),
+                                                    _i64, _p, _p, _i64, _p]),
             "lvsa_attention_exact": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
                                      [ctypes.POINTER(ExactMask),
                                       ctypes.POINTER(_Tensor), _p]),
@@ -224,6 +230,27 @@ class Csr:
         return (np.ctypeslib.as_array(e, shape=(nnz,)).copy() if nnz
                 else np.zeros(0, dtype=np.uint32))
 
+    def pairs(self):
+        """Pair schedule (pair_ptr, block-form words, token-exact words or
+        None) as numpy copies (lvsa_csr_pairs)."""
+        import numpy as np
+        npairs, nw = _i32(), _i64()
+        pp = _pi32()
+        pw = ctypes.POINTER(ctypes.c_uint32)()
+        pe = ctypes.POINTER(ctypes.c_uint32)()
+        _check(lib().lvsa_csr_pairs(self._h, ctypes.byref(npairs), ctypes.byref(nw),
+                                    ctypes.byref(pp), ctypes.byref(pw), ctypes.byref(pe)),
+               "lvsa_csr_pairs")
+        ptr = np.ctypeslib.as_array(pp, shape=(npairs.value + 1,)).copy()
+        n = nw.value
+        words = (np.ctypeslib.as_array(pw, shape=(n,)).copy() if n
+                 else np.zeros(0, dtype=np.uint32))
+        exact = None
+        if pe:
+            exact = (np.ctypeslib.as_array(pe, shape=(n,)).copy() if n
+                     else np.zeros(0, dtype=np.uint32))
+        return ptr, words, exact
+
     def upload(self, stream=None):
         _check(lib().lvsa_csr_upload(self._h, _stream_ptr(stream)), "lvsa_csr_upload")
         return self
@@ -252,35 +279,70 @@ def build_mask(T, P, B, step, params=None, layer=0, exact=False):
     return Csr(h.value)
 
 
-def device_mask(n_tokens, block, row_ptr, col_idx):
-    """BlockMask view over device int32 tensors (row_ptr [nb+1], col_idx)."""
+def pair_buffers(n_tokens, block, device=None, stream=None):
+    """Device int32 tensors (pair_ptr [ceil(nb/2)+1], pair words
+    [ceil(nb/2)*nb]) sized for a device builder's pair schedule, allocated on
+    `stream` (a torch stream, a raw stream handle or None for the current
+    one) so the caching allocator reuses them only after that stream's work."""
+    import torch
     nb = (n_tokens + block - 1) // block
-    return BlockMask(n_tokens, block, nb, row_ptr.data_ptr(), col_idx.data_ptr())
+    npairs = (nb + 1) // 2
+    dev = device or "cuda"
+    if stream is None:
+        s = torch.cuda.current_stream()
+    elif isinstance(stream, int):
+        s = torch.cuda.ExternalStream(stream)
+    else:
+        s = stream
+    with torch.cuda.stream(s):
+        return (torch.empty(npairs + 1, dtype=torch.int32, device=dev),
+                torch.empty(max(npairs * nb, 1), dtype=torch.int32, device=dev))
+
+
+def _mask_with_pairs(mask, tensors):
+    mask._keep = tensors   # keep the device buffers alive with the view
+    return mask
 
 
 def build_mask_device(T, P, B, step, row_ptr, col_idx, params=None, layer=0,
-                      stream=None):
-    """Device LVSA mask builder into int32 device tensors; returns a BlockMask."""
+                      stream=None, pair_ptr=None, pair_word=None):
+    """Device LVSA mask builder into int32 device tensors (the CSR and its
+    pair schedule; pair buffers are allocated when not given); returns a
+    BlockMask."""
     params = params or Params()
+    N = T * P + params.text_tokens
+    if pair_ptr is None or pair_word is None:
+        pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
     _check(lib().lvsa_build_mask_device(T, P, B, step, layer, ctypes.byref(params),
                                         _p(row_ptr.data_ptr()), _p(col_idx.data_ptr()),
-                                        col_idx.numel(), _stream_ptr(stream)),
+                                        col_idx.numel(), _p(pair_ptr.data_ptr()),
+                                        _p(pair_word.data_ptr()), pair_word.numel(),
+                                        _stream_ptr(stream)),
            "lvsa_build_mask_device")
-    return device_mask(T * P + params.text_tokens, B, row_ptr, col_idx)
+    nb = (N + B - 1) // B
+    m = BlockMask(N, B, nb, row_ptr.data_ptr(), col_idx.data_ptr(), pair_ptr.data_ptr(),
+                  pair_word.data_ptr())
+    return _mask_with_pairs(m, (row_ptr, col_idx, pair_ptr, pair_word))
 
 
 def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
-                            stream=None):
+                            stream=None, pair_ptr=None, pair_word=None):
     """Device builder of the token-exact form into device tensors (row_ptr
-    int32 [nb+1], entry int32/uint32 [>= nb*nb]); returns an ExactMask."""
+    int32 [nb+1], entry int32/uint32 [>= nb*nb], and the token-exact pair
+    schedule, allocated when not given); returns an ExactMask."""
     params = params or Params()
+    N = T * P + params.text_tokens
+    if pair_ptr is None or pair_word is None:
+        pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
     _check(lib().lvsa_build_exact_mask_device(
         T, P, B, step, layer, ctypes.byref(params), _p(row_ptr.data_ptr()),
-        _p(entry.data_ptr()), entry.numel(), _stream_ptr(stream)),
+        _p(entry.data_ptr()), entry.numel(), _p(pair_ptr.data_ptr()),
+        _p(pair_word.data_ptr()), pair_word.numel(), _stream_ptr(stream)),
         "lvsa_build_exact_mask_device")
-    N = T * P + params.text_tokens
     nb = (N + B - 1) // B
-    return ExactMask(N, B, nb, P, row_ptr.data_ptr(), entry.data_ptr())
+    m = ExactMask(N, B, nb, P, row_ptr.data_ptr(), entry.data_ptr(), pair_ptr.data_ptr(),
+                  pair_word.data_ptr())
+    return _mask_with_pairs(m, (row_ptr, entry, pair_ptr, pair_word))
 
 
 def _tensor(t):

@@ -65,12 +65,39 @@ struct lvsa_csr {
   std::vector<int32_t> row_ptr;
   std::vector<int32_t> col_idx;
   std::vector<uint32_t> entry;
+  std::vector<int32_t> pair_ptr;   // pair schedule (block words, and
+  std::vector<uint32_t> pair_word; // token-exact words with entry words)
+  std::vector<uint32_t> pair_exact;
+  // Device copies, in one allocation each, sized when first uploaded.
   int32_t* d_row_ptr = nullptr;
   int32_t* d_col_idx = nullptr;
   uint32_t* d_entry = nullptr;
-  int64_t d_col_cap = 0;
-  int64_t d_entry_cap = 0;
+  int32_t* d_pair_ptr = nullptr;
+  uint32_t* d_pair_word = nullptr;
+  uint32_t* d_pair_exact = nullptr;
 };
+
+namespace {
+
+// Device copy of a host array: allocated on the first upload (the handle's
+// arrays never change size), then copied asynchronously on `s`.
+template <typename T>
+lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s) {
+  if (!*dev) {
+    const size_t n = host.empty() ? 1 : host.size();
+    if (hipMalloc(dev, sizeof(T) * n) != hipSuccess) {
+      *dev = nullptr;
+      return LVSA_ENOMEM;
+    }
+  }
+  if (!host.empty() &&
+      hipMemcpyAsync(*dev, host.data(), sizeof(T) * host.size(), hipMemcpyHostToDevice,
+                     s) != hipSuccess)
+    return LVSA_EDEVICE;
+  return LVSA_OK;
+}
+
+}  // namespace
 
 using namespace lvsa;
 
@@ -87,7 +114,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 10300; }
+int32_t lvsa_version(void) { return 10400; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
@@ -146,6 +173,8 @@ lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
   try {
     build_csr_host(c, P, B, &h->row_ptr, &h->col_idx,
                    h->has_entry ? &h->entry : nullptr);
+    build_pairs_host(h->row_ptr, h->col_idx, h->has_entry ? &h->entry : nullptr,
+                     &h->pair_ptr, &h->pair_word, h->has_entry ? &h->pair_exact : nullptr);
   } catch (const std::bad_alloc&) {
     delete h;
     return LVSA_ENOMEM;
@@ -187,70 +216,56 @@ lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
 
 lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
   if (!csr) return LVSA_EINVAL;
-  const int64_t nnz = (int64_t)csr->col_idx.size();
-  if (!csr->d_row_ptr) {
-    if (hipMalloc(&csr->d_row_ptr, sizeof(int32_t) * csr->row_ptr.size()) !=
-        hipSuccess) {
-      csr->d_row_ptr = nullptr;
-      return LVSA_ENOMEM;
-    }
-  }
-  if (!csr->d_col_idx || csr->d_col_cap < nnz) {
-    if (csr->d_col_idx) (void)hipFree(csr->d_col_idx);
-    csr->d_col_idx = nullptr;
-    csr->d_col_cap = 0;
-    const int64_t cap = nnz > 0 ? nnz : 1;
-    if (hipMalloc(&csr->d_col_idx, sizeof(int32_t) * cap) != hipSuccess) {
-      csr->d_col_idx = nullptr;
-      return LVSA_ENOMEM;
-    }
-    csr->d_col_cap = cap;
-  }
-  if (csr->has_entry && (!csr->d_entry || csr->d_entry_cap < nnz)) {
-    if (csr->d_entry) (void)hipFree(csr->d_entry);
-    csr->d_entry = nullptr;
-    csr->d_entry_cap = 0;
-    const int64_t cap = nnz > 0 ? nnz : 1;
-    if (hipMalloc(&csr->d_entry, sizeof(uint32_t) * cap) != hipSuccess) {
-      csr->d_entry = nullptr;
-      return LVSA_ENOMEM;
-    }
-    csr->d_entry_cap = cap;
-  }
   hipStream_t s = (hipStream_t)stream;
-  if (hipMemcpyAsync(csr->d_row_ptr, csr->row_ptr.data(),
-                     sizeof(int32_t) * csr->row_ptr.size(),
-                     hipMemcpyHostToDevice, s) != hipSuccess)
-    return LVSA_EDEVICE;
-  if (nnz > 0 &&
-      hipMemcpyAsync(csr->d_col_idx, csr->col_idx.data(), sizeof(int32_t) * nnz,
-                     hipMemcpyHostToDevice, s) != hipSuccess)
-    return LVSA_EDEVICE;
-  if (csr->has_entry && nnz > 0 &&
-      hipMemcpyAsync(csr->d_entry, csr->entry.data(), sizeof(uint32_t) * nnz,
-                     hipMemcpyHostToDevice, s) != hipSuccess)
-    return LVSA_EDEVICE;
+  lvsa_status st;
+  if ((st = upload_array(csr->row_ptr, &csr->d_row_ptr, s)) != LVSA_OK) return st;
+  if ((st = upload_array(csr->col_idx, &csr->d_col_idx, s)) != LVSA_OK) return st;
+  if ((st = upload_array(csr->pair_ptr, &csr->d_pair_ptr, s)) != LVSA_OK) return st;
+  if ((st = upload_array(csr->pair_word, &csr->d_pair_word, s)) != LVSA_OK) return st;
+  if (csr->has_entry) {
+    if ((st = upload_array(csr->entry, &csr->d_entry, s)) != LVSA_OK) return st;
+    if ((st = upload_array(csr->pair_exact, &csr->d_pair_exact, s)) != LVSA_OK) return st;
+  }
   return LVSA_OK;
 }
 
 void lvsa_csr_free(lvsa_csr* csr) {
   if (!csr) return;
-  if (csr->d_row_ptr || csr->d_col_idx || csr->d_entry) {
+  void* dev[] = {csr->d_row_ptr, csr->d_col_idx, csr->d_entry,
+                 csr->d_pair_ptr, csr->d_pair_word, csr->d_pair_exact};
+  bool any = false;
+  for (void* d : dev) any = any || d != nullptr;
+  if (any) {
     (void)hipDeviceSynchronize();
-    if (csr->d_row_ptr) (void)hipFree(csr->d_row_ptr);
-    if (csr->d_col_idx) (void)hipFree(csr->d_col_idx);
-    if (csr->d_entry) (void)hipFree(csr->d_entry);
+    for (void* d : dev)
+      if (d) (void)hipFree(d);
   }
   delete csr;
 }
 
+lvsa_status lvsa_csr_pairs(const lvsa_csr* csr, int32_t* n_pairs, int64_t* n_words,
+                           const int32_t** pair_ptr, const uint32_t** pair_word,
+                           const uint32_t** pair_exact) {
+  if (!csr) return LVSA_EINVAL;
+  if (n_pairs) *n_pairs = (int32_t)csr->pair_ptr.size() - 1;
+  if (n_words) *n_words = (int64_t)csr->pair_word.size();
+  if (pair_ptr) *pair_ptr = csr->pair_ptr.data();
+  if (pair_word) *pair_word = csr->pair_word.data();
+  if (pair_exact) *pair_exact = csr->has_entry ? csr->pair_exact.data() : nullptr;
+  return LVSA_OK;
+}
+
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out) {
-  if (!csr || !out || !csr->d_row_ptr || !csr->d_col_idx) return LVSA_EINVAL;
+  if (!csr || !out || !csr->d_row_ptr || !csr->d_col_idx || !csr->d_pair_ptr ||
+      !csr->d_pair_word)
+    return LVSA_EINVAL;
   out->n_tokens = csr->n_tokens;
   out->block = csr->block;
   out->n_blocks = csr->n_blocks;
   out->row_ptr = csr->d_row_ptr;
   out->col_idx = csr->d_col_idx;
+  out->pair_ptr = csr->d_pair_ptr;
+  out->pair_word = csr->d_pair_word;
   return LVSA_OK;
 }
 
@@ -266,13 +281,16 @@ lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
 lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out) {
   if (!csr || !out) return LVSA_EINVAL;
   if (!csr->has_entry) return LVSA_EUNSUPPORTED;
-  if (!csr->d_row_ptr || !csr->d_entry) return LVSA_EINVAL;
+  if (!csr->d_row_ptr || !csr->d_entry || !csr->d_pair_ptr || !csr->d_pair_exact)
+    return LVSA_EINVAL;
   out->n_tokens = csr->n_tokens;
   out->block = csr->block;
   out->n_blocks = csr->n_blocks;
   out->frame_tokens = csr->frame_tokens;
   out->row_ptr = csr->d_row_ptr;
   out->entry = csr->d_entry;
+  out->pair_ptr = csr->d_pair_ptr;
+  out->pair_word = csr->d_pair_exact;
   return LVSA_OK;
 }
 
@@ -280,8 +298,11 @@ lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
                                          int32_t step, int32_t layer,
                                          const lvsa_params* p,
                                          int32_t* d_row_ptr, uint32_t* d_entry,
-                                         int64_t entry_capacity, void* stream) {
-  if (layer < 0 || !d_row_ptr || !d_entry) return LVSA_EINVAL;
+                                         int64_t entry_capacity, int32_t* d_pair_ptr,
+                                         uint32_t* d_pair_word, int64_t pair_capacity,
+                                         void* stream) {
+  if (layer < 0 || !d_row_ptr || !d_entry || !d_pair_ptr || !d_pair_word)
+    return LVSA_EINVAL;
   FrameCfg c;
   lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
@@ -290,9 +311,9 @@ lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
   const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (!exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
   if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
-  if (entry_capacity < nb * nb) return LVSA_EINVAL;
-  if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry,
-                               (hipStream_t)stream) != hipSuccess)
+  if (entry_capacity < nb * nb || pair_capacity < (nb + 1) / 2 * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry, d_pair_ptr,
+                               d_pair_word, true, (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -301,8 +322,10 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t step, int32_t layer,
                                    const lvsa_params* p, int32_t* d_row_ptr,
                                    int32_t* d_col_idx, int64_t col_capacity,
-                                   void* stream) {
-  if (layer < 0 || !d_row_ptr || !d_col_idx) return LVSA_EINVAL;
+                                   int32_t* d_pair_ptr, uint32_t* d_pair_word,
+                                   int64_t pair_capacity, void* stream) {
+  if (layer < 0 || !d_row_ptr || !d_col_idx || !d_pair_ptr || !d_pair_word)
+    return LVSA_EINVAL;
   FrameCfg c;
   lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
@@ -310,9 +333,9 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
   if (st != LVSA_OK) return st;
   const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
-  if (col_capacity < nb * nb) return LVSA_EINVAL;
-  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr,
-                               (hipStream_t)stream) != hipSuccess)
+  if (col_capacity < nb * nb || pair_capacity < (nb + 1) / 2 * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr, d_pair_ptr,
+                               d_pair_word, false, (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -332,7 +355,7 @@ lvsa_status check_tensor(const lvsa_tensor* t, int32_t heads, int32_t n) {
 lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                           const lvsa_tensor* v, int32_t n_tokens,
                           int32_t block, int32_t n_blocks,
-                          const int32_t* row_ptr, const int32_t* col_idx,
+                          const int32_t* pair_ptr, const uint32_t* pair_word,
                           int32_t frame_tokens, AttnMode mode,
                           lvsa_tensor* out, void* stream) {
   if (!q || !k || !v || !out) return LVSA_EINVAL;
@@ -371,8 +394,8 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   a.heads = H;
   a.n_tokens = n_tokens;
   a.n_blocks = n_blocks;
-  a.row_ptr = row_ptr;
-  a.col_idx = col_idx;
+  a.pair_ptr = pair_ptr;
+  a.pair_word = pair_word;
   a.frame_tokens = frame_tokens;
   if (launch_attention(a, block, mode, (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
@@ -384,22 +407,22 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream) {
-  if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
+  if (!mask || !mask->pair_ptr || !mask->pair_word) return LVSA_EINVAL;
   return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
-                       mask->row_ptr, mask->col_idx, 0, ATTN_BLOCK, out, stream);
+                       mask->pair_ptr, mask->pair_word, 0, ATTN_BLOCK, out, stream);
 }
 
 lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  const lvsa_tensor* v,
                                  const lvsa_exact_mask* mask, lvsa_tensor* out,
                                  void* stream) {
-  if (!mask || !mask->row_ptr || !mask->entry) return LVSA_EINVAL;
+  if (!mask || !mask->pair_ptr || !mask->pair_word) return LVSA_EINVAL;
   if (mask->frame_tokens < 1) return LVSA_EINVAL;
   if (!exact_supported(mask->frame_tokens, mask->block, mask->n_blocks))
     return LVSA_EUNSUPPORTED;
   return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
-                       mask->row_ptr, (const int32_t*)mask->entry,
-                       mask->frame_tokens, ATTN_EXACT, out, stream);
+                       mask->pair_ptr, mask->pair_word, mask->frame_tokens, ATTN_EXACT,
+                       out, stream);
 }
 
 lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,

@@ -5,29 +5,33 @@
 // (all keys) with the same kernel visiting every key block.
 //
 // Work decomposition
-//   One workgroup per (head, query block of BLOCK rows) with 2*BLOCK/(32*QT)
-//   waves: 8 waves (two per SIMD) at BLOCK = 128 and QT = 1.  Wave w owns
-//   32*QT query rows (row group w % RG, as QT 32-row MFMA tiles) and one half
-//   of the keys of every key block (w / RG).  The two waves of a row group
-//   keep independent online softmax states over disjoint keys and are merged
-//   once at the end.
+//   One workgroup per (head, pair of query blocks 2p and 2p+1): 2*BLOCK query
+//   rows, NW = 2*BLOCK/32 waves (8 at BLOCK = 128) of 32 rows each; waves
+//   0..NW/2-1 hold rows of query block 2p, the others rows of 2p+1.  The
+//   workgroup walks the pair's schedule (the union of the two blocks' key
+//   lists, each word saying which of the two keeps the key block, lvsa.h) one
+//   half key block (KEYS = BLOCK/2 keys) per step, and every wave takes all
+//   KEYS keys of the step for its rows.  Adjacent query blocks mostly keep the
+//   same key blocks (they touch the same frames), so each K/V tile brought
+//   from HBM/L2 into LDS serves 2*BLOCK query rows; a key block that only one
+//   of the two keeps is masked out (no valid keys) for the other's waves.
 //
-// Schedule ("ping-pong", one key block per step)
-//   The two waves of a row group (waves w and w + RG, which share a SIMD when
-//   the workgroup has 8 waves) run half a step apart: while one is in its
-//   GEMM phase (S(j+1) = K(j+1) Q^T and O += P(j) V(j), MFMA with fragments
-//   from LDS) the other is in its softmax phase (row max, exponentials, P in
-//   bf16: VALU), so the matrix core and the VALU of each SIMD are busy at the
-//   same time.  A barrier ends every half step.  LDS holds two K stages and
-//   two V stages (slab layout, see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
+// Schedule ("ping-pong", one half key block per step)
+//   Waves w and w + NW/2 (which share a SIMD when NW = 8) run half a step
+//   apart: while one is in its GEMM phase (O += P(j) V(j), l += row sums of
+//   P(j), S(j+1) = K(j+1) Q^T: MFMA with fragments from LDS) the other is in
+//   its softmax phase (row max, exponentials, P in bf16: VALU), so the matrix
+//   core and the VALU of each SIMD are busy at the same time.  A barrier ends
+//   every half step.  LDS holds two K stages and two V stages (slab layout,
+//   see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
 //   step j-1 with buffer loads that write LDS directly, issued during the
 //   first half of step j and waited for at its end.  The buffer resource's
 //   size bound turns rows at or past N (ragged last block) into zeros.
 //   Row sums come from the matrix core: in the GEMM phase a 16x16x32 MFMA
 //   with a constant 0/1 A operand adds up each 16-key step of P for all 32
-//   rows of the wave.  That takes 32 adds per step off the softmax phase, whose
-//   wave issues its VALU work alone on the SIMD, for 4 small MFMAs (1/16 of
-//   the step's matrix work), and sums exactly the bf16 P that multiplies V.
+//   rows of the wave.  That takes 32 adds per step off the softmax phase, for
+//   4 small MFMAs (1/16 of the step's matrix work), and sums exactly the bf16
+//   P that multiplies V.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
@@ -104,12 +108,11 @@ constexpr int QT = LVSA_QT;   // 32-row query tiles per wave
 
 template <int BLOCK>
 struct Tile {
-  static constexpr int RG = BLOCK / (32 * QT);  // row groups of 32*QT rows
-  static constexpr int NW = 2 * RG;             // waves
-  static constexpr int NT = NW * 64;            // threads
-  static constexpr int KH = BLOCK / 2;          // keys per wave per block
-  static constexpr int KTW = KH / 32;           // 32-key tiles per wave
-  static constexpr int SLAB = BLOCK * SLAB_ROW; // bytes per slab
+  static constexpr int KEYS = BLOCK / 2;            // keys per pipeline step
+  static constexpr int NW = 2 * BLOCK / (32 * QT);  // waves (32*QT query rows each)
+  static constexpr int NT = NW * 64;                // threads
+  static constexpr int KTW = KEYS / 32;             // 32-key tiles per step
+  static constexpr int SLAB = KEYS * SLAB_ROW;      // bytes per slab
   static constexpr int BYTES = 4 * SLAB;        // bytes per tile
   static constexpr int INSTR = BYTES / 1024;    // 1 KiB wave loads per tile
   static constexpr int LOADS = INSTR / NW;      // per wave per tile
@@ -142,15 +145,17 @@ __device__ __forceinline__ void issue_load(uint32_t lds_dst, __amdgpu_buffer_rsr
       : "memory", "m0");
 }
 
-// Buffer resource over rows kb*BLOCK .. N-1 of one head of K or V; a key
-// block index outside [0, nb) yields an empty resource (all loads read 0).
+// Buffer resource over rows sb*KEYS .. N-1 of one head of K or V (sub-block
+// sb = half sb%2 of key block sb/2); an index outside [0, nsb), nsb the
+// number of sub-blocks holding keys below N, yields an empty resource (all
+// loads read 0).
 template <int BLOCK>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const __bf16* head_base,
                                                             int64_t row_elems,
                                                             uint32_t head_bytes,
-                                                            int kb, int nb) {
-  const bool ok = (uint32_t)kb < (uint32_t)nb;
-  const int64_t skip = ok ? (int64_t)kb * BLOCK * row_elems : 0;
+                                                            int sb, int nsb) {
+  const bool ok = (uint32_t)sb < (uint32_t)nsb;
+  const int64_t skip = ok ? (int64_t)sb * Tile<BLOCK>::KEYS * row_elems : 0;
   const uint32_t bytes = ok ? head_bytes - (uint32_t)(skip * 2) : 0u;
   return make_rsrc(head_base + skip, bytes);
 }
@@ -231,14 +236,12 @@ struct FragAddr {
   uint32_t v_lo, v_hi;      // V rows for k-slots 0..3 / 4..7 (transposing read)
 };
 
-template <int BLOCK>
-__device__ __forceinline__ FragAddr frag_addr(int kh, int lane) {
-  using TL = Tile<BLOCK>;
+__device__ __forceinline__ FragAddr frag_addr(int lane) {
   const int hl = lane / 32, li = lane % 32;
   FragAddr f;
-  // K: row KH*kh + 32*kt + li, d = 16*stp + 8*hl: slab stp/2, logical chunk
+  // K: row 32*kt + li, d = 16*stp + 8*hl: slab stp/2, logical chunk
   // 2*(stp%2) + hl.  x(row) = (li/4)%4 for every kt.
-  const int krow = TL::KH * kh + li;
+  const int krow = li;
   const int kx = xsw(krow);
   f.k_even = krow * SLAB_ROW + ((hl ^ kx) * 16);
   f.k_odd = krow * SLAB_ROW + (((2 + hl) ^ kx) * 16);
@@ -248,7 +251,7 @@ __device__ __forceinline__ FragAddr frag_addr(int kh, int lane) {
   // columns 16*(g%2) + 4q .. +3 of the slab (logical chunk 2*(g%2) + q/2,
   // byte half q%2).  Rows +8 hold k-slots 4..7.
   const int g = lane / 16, sl = lane % 16;
-  const int vrow = TL::KH * kh + 4 * (g / 2) + sl / 4;
+  const int vrow = 4 * (g / 2) + sl / 4;
   const int lc = 2 * (g % 2) + (sl % 4) / 2;
   const int half = (sl % 2) * 8;
   f.v_lo = vrow * SLAB_ROW + ((lc ^ xsw(vrow)) * 16) + half;
@@ -256,7 +259,7 @@ __device__ __forceinline__ FragAddr frag_addr(int kh, int lane) {
   return f;
 }
 
-// S^T = K Q^T for this wave's keys of one block (K tile at lds_k).
+// S^T = K Q^T for the keys of one step (K tile at lds_k).
 template <int BLOCK>
 __device__ __forceinline__ void compute_scores(const char* lds_k,
                                                const bf16x8 (&qf)[QT][8],
@@ -290,16 +293,15 @@ struct WaveState {
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
-// -inf.  `valid` = N - first key of the block.
+// -inf.  `valid` = N - first key of the step (0 or less: no key is valid).
 template <int BLOCK>
-__device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int kh, int lane,
-                                          int valid) {
+__device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
-  if (valid < BLOCK) {
+  if (valid < TL::KEYS) {
     // key = lane part + constant part; compare the constant part with a
     // per-lane limit so no per-element key index is kept in a register.
-    const int lim = valid - (TL::KH * kh + 4 * hl);
+    const int lim = valid - 4 * hl;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
@@ -312,22 +314,22 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int kh, int lane,
   }
 }
 
-// Token-exact form: the block's entry word w says which query-frame /
-// key-frame parts are attended (pattern bit 2a+b, a = the lane's query row
-// lies in the query block's second frame, b = the key lies in the key
-// block's second frame, which starts kfirst keys in).  A row's kept keys are
-// then one range [klo, khi) of the block, also clipped at `valid` = N minus
-// the block's first key.  Scores outside it become -inf.  Blocks whose every
-// part is attended and that are not ragged skip the masking.
+// Token-exact form: the 4-bit pattern of the wave's query block for this key
+// block says which query-frame / key-frame parts are attended (bit 2a+b, a =
+// the lane's query row lies in the query block's second frame, b = the key
+// lies in the key block's second frame, which starts kfirst keys in; 0 = the
+// query block does not keep the key block).  A row's kept keys are then one
+// range [klo, khi) of the block, also clipped at `valid` = N minus the
+// block's first key; the step holds keys key0 .. key0+KEYS-1 of the block.
+// Scores outside the range become -inf.  Blocks whose every part is attended
+// and that are not ragged skip the masking.
 template <int BLOCK>
-__device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int kh, int lane,
-                                           uint32_t w, int valid,
+__device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t pat,
+                                           int kfirst, int valid, int key0,
                                            const bool (&second)[QT]) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
-  const uint32_t pat = w >> 24;
   if (pat != 0xFu || valid < BLOCK) {
-    const int kfirst = (int)((w >> 16) & 0xFFu);
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       const uint32_t bits = second[qt] ? pat >> 2 : pat;
@@ -338,7 +340,7 @@ __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int kh, int lane,
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = TL::KH * kh + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
+          const int key = key0 + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
           if ((uint32_t)(key - klo) >= width) sc.s[qt][kt][r] = -__builtin_inff();
         }
     }
@@ -411,69 +413,72 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
                                            const StepLoads<BLOCK>* sl) {
   using TL = Tile<BLOCK>;
   constexpr int NS = 8 * TL::KTW;   // S MFMAs (per q tile): (key tile, d-step)
-  constexpr int NP = 8 * TL::KTW;   // PV fragments: (key tile, k-step half, d tile)
-  static_assert(NS == NP, "interleave");
+  constexpr int NP = 8 * TL::KTW;   // PV fragments: (d tile, key tile, k-step half)
+  constexpr int NF = NS + NP;
   constexpr int AHEAD = 3;
   constexpr int NLOADS = 2 * TL::LOADS;
-  auto kfrag = [&](int i) {
-    const int kt = i / 8, stp = i % 8;
-    const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) + (stp / 2) * TL::SLAB +
-                         kt * 32 * SLAB_ROW;
-    return *(const bf16x8*)(lds_k + off);
-  };
-  auto vfrag = [&](int f) {
-    const int kt = f / 8, c = (f / 4) % 2, dt = f % 4;
+  // Fragment i < NS: K, key tile i/8, d-step i%8.  Fragment NS + f: V^T,
+  // d tile f/(2*KTW), key tile (f/2)%KTW, k-step half f%2 -- so MFMAs on one
+  // accumulator follow each other.
+  auto frag = [&](int i) -> bf16x8 {
+    if (i < NS) {
+      const int kt = i / 8, stp = i % 8;
+      const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) + (stp / 2) * TL::SLAB +
+                           kt * 32 * SLAB_ROW;
+      return *(const bf16x8*)(lds_k + off);
+    }
+    const int f = i - NS;
+    const int dt = f / (2 * TL::KTW), kt = (f / 2) % TL::KTW, c = f % 2;
     const uint32_t off = dt * TL::SLAB + (32 * kt + 16 * c) * SLAB_ROW;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_lo + off));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_hi + off));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  bf16x8 kf[NS], vf[NP];
+  bf16x8 fr[NF];
 #pragma unroll
-  for (int i = 0; i < AHEAD; ++i) {
-    kf[i] = kfrag(i);
-    vf[i] = vfrag(i);
-  }
+  for (int i = 0; i < AHEAD; ++i) fr[i] = frag(i);
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int i = 0; i < NS; ++i) {
-    if (i + AHEAD < NS) {
-      kf[i + AHEAD] = kfrag(i + AHEAD);
-      vf[i + AHEAD] = vfrag(i + AHEAD);
-    }
-    if (sl && i % (NS / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NS / NLOADS));
-    {
+  for (int i = 0; i < NF; ++i) {
+    if (i + AHEAD < NF) fr[i + AHEAD] = frag(i + AHEAD);
+    if (sl && i % (NF / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NF / NLOADS));
+    if (i < NS) {
       const int kt = i / 8, stp = i % 8;
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
         sc.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            kf[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
-    }
-    {
-      const int kt = i / 8, c = (i / 4) % 2, dt = i % 4;
+            fr[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
+    } else {
+      const int f = i - NS;
+      const int dt = f / (2 * TL::KTW), kt = (f / 2) % TL::KTW, c = f % 2;
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
-        st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pr.p[qt][kt][c],
+        st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], pr.p[qt][kt][c],
                                                                st.o[qt][dt], 0, 0, 0);
-      if (dt == 3)
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt][c], st.l[qt],
-                                                             0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+#pragma unroll
+  for (int kt = 0; kt < TL::KTW; ++kt)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+        st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt][c], st.l[qt],
+                                                           0, 0, 0);
 }
 
-// MODE: ATTN_DENSE (every key block), ATTN_BLOCK (kept blocks of a block
-// CSR), ATTN_EXACT (kept blocks, col_idx holding token-exact entry words).
+// MODE: ATTN_DENSE (every key block), ATTN_BLOCK (block schedule words),
+// ATTN_EXACT (token-exact schedule words).  `sched_ptr` / `sched` are the
+// pair schedule (lvsa.h): row p lists the key blocks of query blocks 2p and
+// 2p+1.
 template <int BLOCK, int MODE>
 __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
     const __bf16* __restrict__ vg, __bf16* __restrict__ og, int64_t q_sh,
     int64_t q_st, int64_t k_sh, int64_t k_st, int64_t v_sh, int64_t v_st,
     int64_t o_sh, int64_t o_st, int32_t H, int32_t N, int32_t nb,
-    const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
+    const int32_t* __restrict__ sched_ptr, const uint32_t* __restrict__ sched,
     int32_t P, float scale_log2) {
   using TL = Tile<BLOCK>;
   constexpr bool SPARSE = MODE != ATTN_DENSE;
@@ -487,12 +492,14 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const int lane = tid % 64;
   const int hl = lane / 32;
   const int li = lane % 32;
-  const int rg = wave % TL::RG;  // row group
-  const int kh = wave / TL::RG;  // key half
 
-  const int tile = xcd_remap(blockIdx.x, nb * H);
-  const int head = tile / nb;
-  const int qb = tile % nb;
+  const int npairs = (nb + 1) / 2;
+  const int tile = xcd_remap(blockIdx.x, npairs * H);
+  const int head = tile / npairs;
+  const int pq = tile % npairs;                 // query blocks 2pq, 2pq+1
+  const bool upper = wave >= TL::NW / 2;        // rows of query block 2pq+1
+  const int qb = 2 * pq + (upper ? 1 : 0);
+  const int rows0 = 32 * QT * (wave % (TL::NW / 2));   // first row within qb
 
   const __bf16* qh = qg + head * q_sh;
   __bf16* oh = og + head * o_sh;
@@ -502,18 +509,22 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const uint32_t v_bytes = (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2);
   const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
   const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
-  // Key-block values below are block indices, or entry words in exact mode.
-  auto kb_of = [&](int w) { return EXACT ? (int)((uint32_t)w & 0xFFFFu) : w; };
-  auto rk_at = [&](int w) {
-    return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, kb_of(w), nb);
+  // Schedule words: key block in bits 0..29 (block form) or 0..15 (exact
+  // form); step j takes half j%2 of the j/2-th word's key block.
+  auto kb_of = [&](uint32_t w) {
+    return (int)(EXACT ? (w & 0xFFFFu) : (w & 0x3FFFFFFFu));
   };
-  auto rv_at = [&](int w) {
-    return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, kb_of(w), nb);
+  const int nsb = (N + TL::KEYS - 1) / TL::KEYS;   // sub-blocks holding keys < N
+  auto rk_at = [&](uint32_t w, int half) {
+    return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, 2 * kb_of(w) + half, nsb);
   };
-  const FragAddr fa = frag_addr<BLOCK>(kh, lane);
+  auto rv_at = [&](uint32_t w, int half) {
+    return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, 2 * kb_of(w) + half, nsb);
+  };
+  const FragAddr fa = frag_addr(lane);
 
   // Q fragments: rows qrow0 + 32*qt, k-slots d = 16*stp + 8*hl + 0..7.
-  const int qrow0 = qb * BLOCK + 32 * QT * rg + li;
+  const int qrow0 = qb * BLOCK + rows0 + li;
   bf16x8 qf[QT][8];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
@@ -534,30 +545,39 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   if constexpr (EXACT) {
     const int qfirst = P - (int)(((int64_t)qb * BLOCK) % P);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) second[qt] = qrow0 + 32 * qt - qb * BLOCK >= qfirst;
+    for (int qt = 0; qt < QT; ++qt) second[qt] = rows0 + 32 * qt + li >= qfirst;
   }
-  auto mask_block = [&](Scores<BLOCK>& sc, int w) {
+  // Masks the scores of step `half` of schedule word w for this wave's query
+  // block: a key block that block does not keep has no valid keys.
+  const uint32_t kept_bit = upper ? 31u : 30u;       // block form
+  const uint32_t pat_shift = upper ? 28u : 24u;      // exact form
+  auto mask_block = [&](Scores<BLOCK>& sc, uint32_t w, int half) {
+    const int kb = kb_of(w);
     if constexpr (EXACT)
-      mask_exact<BLOCK>(sc, kh, lane, (uint32_t)w, N - kb_of(w) * BLOCK, second);
+      mask_exact<BLOCK>(sc, lane, (w >> pat_shift) & 0xFu, (int)((w >> 16) & 0xFFu),
+                        N - kb * BLOCK, TL::KEYS * half, second);
     else
-      mask_tail<BLOCK>(sc, kh, lane, N - w * BLOCK);
+      mask_tail<BLOCK>(sc, lane,
+                       ((w >> kept_bit) & 1u) ? N - (2 * kb + half) * TL::KEYS : 0);
   };
 
-  int beg = 0, n = nb;
+  int beg = 0, n = 2 * nb;
   if constexpr (SPARSE) {
-    beg = row_ptr[qb];
-    n = row_ptr[qb + 1] - beg;
+    beg = sched_ptr[pq];
+    n = 2 * (sched_ptr[pq + 1] - beg);
   }
-  auto kb_at = [&](int j) { return SPARSE ? col_idx[beg + j] : j; };
-  // Key block j+3 is fetched by a vector load one step before it is needed,
-  // so the load's latency hides under a whole step (a scalar load would be
-  // waited for at the next LDS wait, which shares its counter).
-  const __amdgpu_buffer_rsrc_t rci =
-      make_rsrc(col_idx, SPARSE ? (uint32_t)(row_ptr[nb] * 4) : 0u);
-  auto kb_fetch = [&](int j) -> int {   // VGPR value, clamped to the row
-    if constexpr (!SPARSE) return j < n ? j : n - 1;
+  auto word_at = [&](int j) -> uint32_t {   // schedule word of step j
+    return SPARSE ? sched[beg + j / 2] : ((uint32_t)(j / 2) | 0xC0000000u);
+  };
+  // The word of step j+3 is fetched by a vector load one step before it is
+  // needed, so the load's latency hides under a whole step (a scalar load
+  // would be waited for at the next LDS wait, which shares its counter).
+  const __amdgpu_buffer_rsrc_t rsched =
+      make_rsrc(sched, SPARSE ? (uint32_t)(sched_ptr[npairs] * 4) : 0u);
+  auto word_fetch = [&](int j) -> uint32_t {   // VGPR value, clamped to the row
     const int jj = j < n ? j : n - 1;
-    return __builtin_amdgcn_raw_buffer_load_b32(rci, (beg + jj) * 4, 0, 0);
+    if constexpr (!SPARSE) return (uint32_t)(jj / 2) | 0xC0000000u;
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsched, (beg + jj / 2) * 4, 0, 0);
   };
 
   WaveState<BLOCK> ws;
@@ -585,41 +605,42 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const char* const k_lds = lds;
     const char* const v_lds = lds + 2 * TL::BYTES;
 
-    // Ping-pong schedule.  The waves of key half 0 ("leaders") run half a
-    // step ahead of those of key half 1, so on each SIMD one wave is in its
-    // GEMM phase (S(j+1) = K(j+1) Q^T and O += P(j) V(j), MFMA) while the
-    // other is in its softmax phase (VALU): half-period 2j is the leaders'
-    // GEMM j and the others' softmax j, half-period 2j+1 the leaders' softmax
-    // j+1 and the others' GEMM j.  A barrier ends every half-period.  K(j+1)
-    // and V(j) stay resident through half-periods 2j and 2j+1; K(j+2) and
-    // V(j+1) are issued in half-period 2j (into the slots of K(j) and V(j-1),
-    // free since half-period 2j-1) and waited for at the end of 2j+1.
-    const bool lead = kh == 0;
-    int kb0 = kb_at(0);
-    int kb1 = n > 1 ? kb_at(1) : kb0;          // block j+1
-    int kb2 = n > 2 ? kb_at(2) : kb1;          // block j+2
-    issue_tile<BLOCK>(k_slot0, rk_at(kb0), kp);
-    issue_tile<BLOCK>(v_slot0, rv_at(kb0), vp);
-    issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(kb1), kp);
+    // Ping-pong schedule.  The waves of query block 2pq ("leaders") run half
+    // a step ahead of those of 2pq+1, so on each SIMD one wave is in its GEMM
+    // phase (O += P(j) V(j), S(j+1) = K(j+1) Q^T: MFMA) while the other is in
+    // its softmax phase (VALU): half-period 2j is the leaders' GEMM j and the
+    // others' softmax j, half-period 2j+1 the leaders' softmax j+1 and the
+    // others' GEMM j.  A barrier ends every half-period.  K(j+1) and V(j) stay
+    // resident through half-periods 2j and 2j+1; K(j+2) and V(j+1) are issued
+    // in half-period 2j (into the slots of K(j) and V(j-1), free since
+    // half-period 2j-1) and waited for at the end of 2j+1.
+    const bool lead = !upper;
+    const uint32_t w0 = word_at(0);
+    uint32_t w1 = n > 1 ? word_at(1) : w0;     // step j+1
+    uint32_t w2 = n > 2 ? word_at(2) : w1;     // step j+2
+    issue_tile<BLOCK>(k_slot0, rk_at(w0, 0), kp);
+    issue_tile<BLOCK>(v_slot0, rv_at(w0, 0), vp);
+    issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(w1, 1), kp);
     wait_loads_and_sync();
     Scores<BLOCK> sc;
     compute_scores<BLOCK>(k_lds, qf, sc, fa);   // S(0)
-    mask_block(sc, kb0);
+    mask_block(sc, w0, 0);
     Probs<BLOCK> pr;
     if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
     __syncthreads();
     for (int j = 0; j < n; ++j) {
-      const int kb3v = kb_fetch(j + 3);
+      const uint32_t w3v = word_fetch(j + 3);
+      const int h1 = (j + 1) & 1, h2 = j & 1;    // halves of steps j+1, j+2
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
-          rk_at(kb2), rv_at(kb1), &kp, &vp};
+          rk_at(w2, h2), rv_at(w1, h1), &kp, &vp};
       const char* const kj1 = k_lds + ((j + 1) & 1) * TL::BYTES;   // K(j+1)
       const char* const vj = v_lds + (j & 1) * TL::BYTES;          // V(j)
       // half-period 2j
       if (lead) {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, &sl);
-        mask_block(sc, kb1);
+        mask_block(sc, w1, h1);
       } else {
         softmax_phase<BLOCK>(sc, ws, pr, scale_log2, &sl);
       }
@@ -629,70 +650,39 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
         if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
       } else {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
-        mask_block(sc, kb1);
+        mask_block(sc, w1, h1);
       }
       wait_loads_and_sync();
-      kb1 = kb2;
-      kb2 = __builtin_amdgcn_readfirstlane(kb3v);
+      w1 = w2;
+      w2 = __builtin_amdgcn_readfirstlane(w3v);
     }
     __syncthreads();
   }
 
-  // Merge the two key halves of each row group: the second-half wave leaves
-  // its state in LDS (O as [register][lane] floats, conflict-free), the
-  // first-half wave combines and stores.
-  float* mo = (float*)lds;                      // [RG][QT*64 regs][64 lanes]
-  float* mm = mo + TL::RG * QT * 64 * 64;       // [RG][QT][64 lanes] max
-  float* ml = mm + TL::RG * QT * 64;            // [RG][QT][64 lanes] pair sums
+  // Every wave holds whole rows: O / l, rounded to bf16.  The l tile holds
+  // row c in register 0 of lane c and row c + 16 in register 1 (c < 16).
   float lsum[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const float r0 = __shfl(ws.l[qt][0], li), r1 = __shfl(ws.l[qt][1], li & 15);
     lsum[qt] = li < 16 ? r0 : r1;
   }
-  if (kh == 1) {
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
+    const float inv = lsum[qt] > 0.f ? 1.f / lsum[qt] : 0.f;
+    const int qrow = qrow0 + 32 * qt;
+    if (qrow < N) {
+      __bf16* orow = oh + (int64_t)qrow * o_st;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          mo[((rg * QT + qt) * 64 + dt * 16 + r) * 64 + lane] = ws.o[qt][dt][r];
-      mm[(rg * QT + qt) * 64 + lane] = ws.m[qt];
-      ml[(rg * QT + qt) * 64 + lane] = lsum[qt];
-    }
-  }
-  __syncthreads();
-  if (kh == 0) {
+        for (int a = 0; a < 4; ++a) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          bf16x4 w;
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      const float m1 = mm[(rg * QT + qt) * 64 + lane];
-      const float l1 = ml[(rg * QT + qt) * 64 + lane];
-      const float m0 = ws.m[qt];
-      const float m = fmaxf(m0, m1);
-      const float a0 = m0 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m0 - m);
-      const float a1 = m1 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(m1 - m);
-      const float ltot = lsum[qt] * a0 + l1 * a1;
-      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-      const float c0 = a0 * inv, c1 = a1 * inv;
-      const int qrow = qrow0 + 32 * qt;
-      if (qrow < N) {
-        __bf16* orow = oh + (int64_t)qrow * o_st;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-            bf16x4 w;
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-              const int r = 4 * a + b;
-              w[b] = (__bf16)(ws.o[qt][dt][r] * c0 +
-                              mo[((rg * QT + qt) * 64 + dt * 16 + r) * 64 + lane] * c1);
-            }
-            *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
-          }
-      }
+          for (int b = 0; b < 4; ++b) w[b] = (__bf16)(ws.o[qt][dt][4 * a + b] * inv);
+          *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
+        }
     }
   }
 }
@@ -700,13 +690,13 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
 template <int BLOCK, int MODE>
 hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)D);
-  const int grid = a.n_blocks * a.heads;
+  const int grid = (a.n_blocks + 1) / 2 * a.heads;
   hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, MODE>), dim3(grid),
                      dim3(Tile<BLOCK>::NT), 0, stream, (const __bf16*)a.q,
                      (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
                      a.q_sh, a.q_st, a.k_sh, a.k_st, a.v_sh, a.v_st, a.o_sh,
-                     a.o_st, a.heads, a.n_tokens, a.n_blocks, a.row_ptr,
-                     a.col_idx, a.frame_tokens, scale_log2);
+                     a.o_st, a.heads, a.n_tokens, a.n_blocks, a.pair_ptr,
+                     a.pair_word, a.frame_tokens, scale_log2);
   return hipGetLastError();
 }
 

@@ -150,6 +150,20 @@ __host__ __device__ inline uint32_t exact_entry(int32_t kb, int32_t f0,
   return exact_word(kb, g0, g1, kfirst, f0, f1, attends);
 }
 
+// Pair schedule words (lvsa.h, "pair schedule"): key block kb listed for the
+// query-block pair (2p, 2p+1), with which of the two keeps it.
+__host__ __device__ inline uint32_t pair_word_of(int32_t kb, bool kept0, bool kept1) {
+  return (uint32_t)kb | (kept0 ? 1u << 30 : 0u) | (kept1 ? 1u << 31 : 0u);
+}
+
+// Token-exact pair word from the entry words e0 of (2p, kb) and e1 of
+// (2p+1, kb), each 0 when that query block does not keep kb (a kept block's
+// pattern is never 0): kb and kfirst, then the two 4-bit patterns.
+__host__ __device__ inline uint32_t pair_exact_word(uint32_t e0, uint32_t e1) {
+  const uint32_t base = (e0 != 0u ? e0 : e1) & 0xFFFFFFu;
+  return base | (((e0 >> 24) & 0xFu) << 24) | (((e1 >> 24) & 0xFu) << 28);
+}
+
 // Whether a block mask of (P, B, nb) can carry exact entry words.
 __host__ __device__ inline bool exact_supported(int32_t P, int32_t B,
                                                 int64_t nb) {

@@ -19,7 +19,11 @@
 //
 // The token-exact entry words (lvsa.h) are built alongside when asked for:
 // one word per kept block, from the two (at most) frames of each side.
+//
+// The attention kernel walks query blocks in pairs; build_pairs_host merges
+// each pair of CSR rows into the pair schedule it reads.
 #include <algorithm>
+#include <climits>
 #include <cstring>
 
 #include "internal.h"
@@ -106,6 +110,42 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
     std::memcpy(col_idx->data() + dst, uniq.data() + src[qb], len * sizeof(int32_t));
     if (entry)
       std::memcpy(entry->data() + dst, uniq_e.data() + src[qb], len * sizeof(uint32_t));
+  }
+}
+
+// Pair schedule: rows 2p and 2p+1 of the CSR merged (both ascending, no
+// repeats), each key block tagged with the rows that hold it.
+void build_pairs_host(const std::vector<int32_t>& row_ptr,
+                      const std::vector<int32_t>& col_idx,
+                      const std::vector<uint32_t>* entry,
+                      std::vector<int32_t>* pair_ptr,
+                      std::vector<uint32_t>* pair_word,
+                      std::vector<uint32_t>* pair_exact) {
+  const int32_t nb = (int32_t)row_ptr.size() - 1;
+  const int32_t npairs = (nb + 1) / 2;
+  const bool exact = entry != nullptr && pair_exact != nullptr;
+  pair_ptr->assign(npairs + 1, 0);
+  pair_word->clear();
+  if (exact) pair_exact->clear();
+  pair_word->reserve(col_idx.size());
+  if (exact) pair_exact->reserve(col_idx.size());
+  for (int32_t p = 0; p < npairs; ++p) {
+    int64_t i = row_ptr[2 * p];
+    const int64_t ie = row_ptr[2 * p + 1];
+    int64_t k = 2 * p + 1 < nb ? row_ptr[2 * p + 1] : 0;
+    const int64_t ke = 2 * p + 1 < nb ? row_ptr[2 * p + 2] : 0;
+    while (i < ie || k < ke) {
+      const int32_t x = i < ie ? col_idx[i] : INT32_MAX;
+      const int32_t y = k < ke ? col_idx[k] : INT32_MAX;
+      const int32_t kb = x < y ? x : y;
+      const bool in0 = x == kb, in1 = y == kb;
+      pair_word->push_back(pair_word_of(kb, in0, in1));
+      if (exact)
+        pair_exact->push_back(pair_exact_word(in0 ? (*entry)[i] : 0u, in1 ? (*entry)[k] : 0u));
+      if (in0) ++i;
+      if (in1) ++k;
+    }
+    (*pair_ptr)[p + 1] = (int32_t)pair_word->size();
   }
 }
 

@@ -12,6 +12,7 @@ import pytest
 import paper_2605_31057_amd as L
 from paper_2605_31057_amd.inputs import WORKLOADS
 from oracle import mask as M
+from tests.pair_util import expected_pairs
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -29,7 +30,7 @@ def _declared_functions():
 def test_library_exports_every_declared_symbol():
     names = _declared_functions()
     assert {"lvsa_build_mask", "lvsa_attention", "lvsa_dense_attention",
-            "lvsa_build_mask_device"} <= names
+            "lvsa_build_mask_device", "lvsa_csr_pairs"} <= names
     lib = ctypes.CDLL(L.LIB_PATH)
     missing = [n for n in sorted(names) if not hasattr(lib, n)]
     assert not missing, missing
@@ -138,6 +139,34 @@ def _status(fn, *args):
     return fn(*args)
 
 
+PAIR_CASES = [  # T, P, B, step, text: even and odd nb, ragged tails, B = 64
+    (121, 1560, 128, 10, 0), (21, 1560, 128, 3, 0), (7, 300, 128, 1, 0),
+    (5, 200, 128, 0, 77), (9, 150, 64, 2, 0), (3, 50, 128, 0, 0), (1, 100, 128, 0, 0),
+]
+
+
+@pytest.mark.parametrize("T,P,B,s,Lt", PAIR_CASES)
+def test_pair_schedule_merges_csr_rows(T, P, B, s, Lt):
+    """Bit for bit: the host pair schedule against its definition applied to
+    the oracle's CSR (block form) and to the handle's entry words (exact)."""
+    p = L.Params(text_tokens=Lt) if T >= 21 else L.Params(budget_frames=0, window=1,
+                                                          tper=3, text_tokens=Lt)
+    csr = L.build_mask(T, P, B, s, p, exact=P >= B)
+    want_rp, want_ci = M.build_mask(T, P, B, s, **_oracle_kw(p))
+    entry = csr.entries() if P >= B else None
+    ptr, words, exact = csr.pairs()
+    e_ptr, e_words, e_exact = expected_pairs(want_rp, want_ci, entry)
+    assert ptr.tolist() == e_ptr
+    assert words.tolist() == e_words
+    if entry is None:
+        assert exact is None
+    else:
+        assert exact.tolist() == e_exact
+    # Every pair row holds its two CSR rows (no block lost, none added).
+    nb = len(want_rp) - 1
+    assert len(ptr) == -(-nb // 2) + 1 and ptr[-1] <= len(want_ci)
+
+
 def test_invalid_mask_arguments():
     lib = L.lib()
     out = ctypes.c_void_p()
@@ -176,13 +205,15 @@ def test_device_builder_rejects_before_launch():
     p = L.Params()
     fake = ctypes.c_void_p(0x1000)
     nb = 1475
-    # capacity below nb*nb
-    assert lib.lvsa_build_mask_device(121, 1560, 128, 0, 0, ctypes.byref(p), fake, fake,
-                                      nb * nb - 1, None) == L.EINVAL
-    assert lib.lvsa_build_mask_device(121, 1560, 128, 0, 0, ctypes.byref(p), None, fake,
-                                      nb * nb, None) == L.EINVAL
-    assert lib.lvsa_build_mask_device(121, 1560, 128, -3, 0, ctypes.byref(p), fake, fake,
-                                      nb * nb, None) == L.EINVAL
+    pc = (nb + 1) // 2 * nb
+    build = lambda rp, ci, cap, pp, pw, pcap, step=0: lib.lvsa_build_mask_device(
+        121, 1560, 128, step, 0, ctypes.byref(p), rp, ci, cap, pp, pw, pcap, None)
+    assert build(fake, fake, nb * nb - 1, fake, fake, pc) == L.EINVAL   # CSR capacity
+    assert build(fake, fake, nb * nb, fake, fake, pc - 1) == L.EINVAL   # pair capacity
+    assert build(None, fake, nb * nb, fake, fake, pc) == L.EINVAL
+    assert build(fake, fake, nb * nb, None, fake, pc) == L.EINVAL
+    assert build(fake, fake, nb * nb, fake, None, pc) == L.EINVAL
+    assert build(fake, fake, nb * nb, fake, fake, pc, step=-3) == L.EINVAL
 
 
 def test_csr_device_view_requires_upload():
@@ -200,7 +231,7 @@ def test_attention_rejects_before_launch():
     lib = L.lib()
     ref = ctypes.byref
     nb = -(-1000 // 128)
-    m = L.BlockMask(1000, 128, nb, 0x2000, 0x3000)
+    m = L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0x5000, 0x6000)
     q, k, v = _t(0x10000), _t(0x20000), _t(0x30000)
     o = _t(0x40000)
     cases = [
@@ -210,9 +241,10 @@ def test_attention_rejects_before_launch():
         (dict(q=_t(0x10008)), L.EUNSUPPORTED),           # alignment
         (dict(k=_t(0x20000, st=132)), L.EUNSUPPORTED),   # token stride % 8
         (dict(o=_t(0x10000)), L.EINVAL),                 # out aliases q
-        (dict(m=L.BlockMask(1000, 96, 11, 0x2000, 0x3000)), L.EUNSUPPORTED),
-        (dict(m=L.BlockMask(1000, 128, nb + 1, 0x2000, 0x3000)), L.EINVAL),
-        (dict(m=L.BlockMask(1000, 128, nb, 0, 0x3000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 96, 11, 0x2000, 0x3000, 0x5000, 0x6000)), L.EUNSUPPORTED),
+        (dict(m=L.BlockMask(1000, 128, nb + 1, 0x2000, 0x3000, 0x5000, 0x6000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0, 0x6000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0x5000, 0)), L.EINVAL),
     ]
     for over, want in cases:
         a = dict(q=q, k=k, v=v, o=o, m=m)
@@ -327,20 +359,23 @@ def test_exact_attention_and_builder_reject_before_launch():
     p = L.Params()
     fake = ctypes.c_void_p(0x1000)
     nb = 1475
-    assert lib.lvsa_build_exact_mask_device(121, 1560, 128, 0, 0, ref(p), fake, fake,
-                                            nb * nb - 1, None) == L.EINVAL
-    assert lib.lvsa_build_exact_mask_device(121, 100, 128, 0, 0, ref(p), fake, fake,
-                                            1 << 30, None) == L.EUNSUPPORTED
-    assert lib.lvsa_build_exact_mask_device(121, 1560, 128, 0, 0, ref(p), fake, None,
-                                            nb * nb, None) == L.EINVAL
+    pc = (nb + 1) // 2 * nb
+    build = lambda P, rp, e, cap, pp, pw, pcap: lib.lvsa_build_exact_mask_device(
+        121, P, 128, 0, 0, ref(p), rp, e, cap, pp, pw, pcap, None)
+    assert build(1560, fake, fake, nb * nb - 1, fake, fake, pc) == L.EINVAL
+    assert build(1560, fake, fake, nb * nb, fake, fake, pc - 1) == L.EINVAL
+    assert build(100, fake, fake, 1 << 30, fake, fake, 1 << 30) == L.EUNSUPPORTED
+    assert build(1560, fake, None, nb * nb, fake, fake, pc) == L.EINVAL
+    assert build(1560, fake, fake, nb * nb, fake, None, pc) == L.EINVAL
     n = 1000
     nbk = -(-n // 128)
     q, k, v, o = _t(0x10000), _t(0x20000), _t(0x30000), _t(0x40000)
+    em = lambda P, B, nb_, pw=0x6000: L.ExactMask(n, B, nb_, P, 0x2000, 0x3000, 0x5000, pw)
     cases = [
-        (L.ExactMask(n, 128, nbk, 100, 0x2000, 0x3000), L.EUNSUPPORTED),  # P < B
-        (L.ExactMask(n, 128, nbk, 0, 0x2000, 0x3000), L.EINVAL),      # P < 1
-        (L.ExactMask(n, 128, nbk, 200, 0x2000, 0), L.EINVAL),         # no entries
-        (L.ExactMask(n, 96, 11, 200, 0x2000, 0x3000), L.EUNSUPPORTED),  # block
+        (em(100, 128, nbk), L.EUNSUPPORTED),        # P < B
+        (em(0, 128, nbk), L.EINVAL),                # P < 1
+        (em(200, 128, nbk, pw=0), L.EINVAL),        # no pair words
+        (em(200, 96, 11), L.EUNSUPPORTED),          # block
     ]
     for m, want in cases:
         assert lib.lvsa_attention_exact(ref(q), ref(k), ref(v), ref(m), ref(o),

@@ -131,9 +131,11 @@ def test_device_exact_builder_matches_host(name):
     p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
     rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
     ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    pp = torch.empty((nb + 1) // 2 + 1, dtype=torch.int32, device="cuda")
+    pw = torch.empty((nb + 1) // 2 * nb, dtype=torch.int32, device="cuda")
     for step in (0, 3, 10):
         _say(f"[exact-builder] {name} step {step}")
-        L.build_exact_mask_device(T, P, B, step, rp, ent, p)
+        L.build_exact_mask_device(T, P, B, step, rp, ent, p, pair_ptr=pp, pair_word=pw)
         torch.cuda.synchronize()
         csr = L.build_mask(T, P, B, step, p, exact=True)
         hrp, _ = csr.arrays()
@@ -141,6 +143,10 @@ def test_device_exact_builder_matches_host(name):
         assert np.array_equal(rp.cpu().numpy(), hrp)
         got = ent[:int(hrp[-1])].cpu().numpy().view(np.uint32)
         assert np.array_equal(got, he)
+        # token-exact pair schedule, bit for bit against the host's
+        hpp, _, hpe = csr.pairs()
+        assert np.array_equal(pp.cpu().numpy(), hpp)
+        assert np.array_equal(pw[:int(hpp[-1])].cpu().numpy().view(np.uint32), hpe)
 
 
 def test_exact_with_device_built_mask_and_determinism():

@@ -32,13 +32,17 @@ def test_step_in_hip_graph_replays_match_eager():
     rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
     ci = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
     ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    pp, pw = L.pair_buffers(N, B)          # schedules, allocated outside the capture
+    ppx, pwx = L.pair_buffers(N, B)
     out = torch.empty_like(q)
     out_x = torch.empty_like(q)
 
     def run(stream):
-        m = L.build_mask_device(T, P, B, step, rp, ci, params=p, stream=stream)
+        m = L.build_mask_device(T, P, B, step, rp, ci, params=p, stream=stream,
+                                pair_ptr=pp, pair_word=pw)
         L.attention(q, k, v, m, out=out, stream=stream)
-        me = L.build_exact_mask_device(T, P, B, step, rp, ent, params=p, stream=stream)
+        me = L.build_exact_mask_device(T, P, B, step, rp, ent, params=p, stream=stream,
+                                       pair_ptr=ppx, pair_word=pwx)
         L.attention_exact(q, k, v, me, out=out_x, stream=stream)
 
     side = torch.cuda.Stream()

@@ -13,6 +13,7 @@ from paper_2605_31057_amd.inputs import WORKLOADS, make_qkv
 from oracle import attention as OA
 from oracle import mask as M
 from tests.gpu_util import assert_close
+from tests.pair_util import expected_pairs
 
 pytestmark = pytest.mark.gpu
 
@@ -28,11 +29,18 @@ def _device_csr(T, P, B, step, p, layer=0):
     nb = -(-(T * P + p.text_tokens) // B)
     rp = torch.full((nb + 1,), -1, dtype=torch.int32, device="cuda")
     ci = torch.full((nb * nb,), -1, dtype=torch.int32, device="cuda")
-    L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer)
+    pp = torch.full(((nb + 1) // 2 + 1,), -1, dtype=torch.int32, device="cuda")
+    pw = torch.full(((nb + 1) // 2 * nb,), -1, dtype=torch.int32, device="cuda")
+    L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer, pair_ptr=pp,
+                        pair_word=pw)
     torch.cuda.synchronize()
     rp = rp.cpu()
     nnz = int(rp[-1])
-    return rp.tolist(), ci[:nnz].cpu().tolist(), ci
+    pp = pp.cpu()
+    words = pw[:int(pp[-1])].cpu().numpy().view(np.uint32)
+    # nothing written past the pair words either
+    assert bool((pw[int(pp[-1]):] == -1).all())
+    return rp.tolist(), ci[:nnz].cpu().tolist(), ci, (pp.tolist(), words.tolist())
 
 
 def _kw(p):
@@ -50,11 +58,14 @@ def test_device_builder_matches_oracle_workloads(name):
     print(f"[mask] {name} steps {steps[0]}..{steps[-1]}", flush=True)
     for s in steps:
         for layer in w.layers:
-            rp, ci, raw = _device_csr(w.frames, w.tokens_per_frame, w.block, s, p, layer)
+            rp, ci, raw, (pp, pw) = _device_csr(w.frames, w.tokens_per_frame, w.block, s,
+                                                p, layer)
             want_rp, want_ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, s,
                                             layer=layer, **_kw(p))
             assert rp == want_rp, (name, s, layer)
             assert ci == want_ci, (name, s, layer)
+            e_pp, e_pw, _ = expected_pairs(want_rp, want_ci)
+            assert pp == e_pp and pw == e_pw, (name, s, layer)
             # nothing written past nnz
             assert bool((raw[len(ci):] == -1).all())
 
@@ -73,9 +84,11 @@ def test_device_builder_matches_oracle_random(mode):
         if -(-(T * P) // B) > 1500:
             B = 64
         s = rng.randint(0, 40)
-        rp, ci, _ = _device_csr(T, P, B, s, p)
+        rp, ci, _, (pp, pw) = _device_csr(T, P, B, s, p)
         want_rp, want_ci = M.build_mask(T, P, B, s, **_kw(p))
         assert rp == want_rp and ci == want_ci, (T, P, B, s)
+        e_pp, e_pw, _ = expected_pairs(want_rp, want_ci)
+        assert pp == e_pp and pw == e_pw, (T, P, B, s)
 
 
 def test_device_mask_attention_equals_host_mask_attention():
@@ -120,8 +133,9 @@ def test_pattern_variant_attention_parity(mode, rotate, extra):
     for s in (1, 2):
         kw = _kw(p)
         rp, ci = M.build_mask(T, P, B, s, **kw)
-        drp, dci, _ = _device_csr(T, P, B, s, p)
+        drp, dci, _, (dpp, dpw) = _device_csr(T, P, B, s, p)
         assert drp == rp and dci == ci
+        assert (dpp, dpw) == expected_pairs(rp, ci)[:2]
         csr = L.build_mask(T, P, B, s, p, exact=True)
         csr.upload()
         blk = L.attention(qd, kd, vd, csr.device_mask())
