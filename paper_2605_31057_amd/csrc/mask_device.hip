@@ -6,16 +6,18 @@
 // trip, so a denoising loop can rebuild the mask for step s on the stream
 // that then runs attention.
 //
-// Two rounds of three launches on the stream, first over the CSR rows (one
-// per query block), then over the pair rows (one per query-block pair 2p,
-// 2p+1: a key block is listed when either block keeps it):
-//   1. one workgroup per row: the windows of the row's frames (Alg. 1) into
-//      LDS, then every key block tested in parallel; the count of listed
-//      blocks goes to row_ptr[r + 1];
-//   2. one workgroup: in-place inclusive scan of the counts;
-//   3. one workgroup per row: the same test again, listed key blocks
+// Four launches on the stream, each workgroup handling a pair of query
+// blocks 2p and 2p+1 (the last pair of an odd nb has one): the CSR rows of
+// both blocks and the pair row (a key block is listed when either keeps it)
+// come from the same tests:
+//   1. one workgroup per pair: the windows of the pair's frames (Alg. 1) into
+//      LDS, then every key block tested in parallel against both query
+//      blocks; the three row lengths go to row_ptr[qb + 1] and pair_ptr[p + 1];
+//   2, 3. one workgroup each: in-place inclusive scans of row_ptr and pair_ptr;
+//   4. one workgroup per pair: the same tests again, listed key blocks
 //      compacted in ascending order (wave ballots and a per-chunk prefix) and
-//      written as block indices, token-exact entry words or pair words.
+//      written as block indices and/or token-exact entry words (CSR) and as
+//      pair words.
 // Every thread tests its own candidates with closed-form rules, so a row
 // costs a few passes over nb candidates whatever its length.
 #include "internal.h"
@@ -32,18 +34,10 @@ constexpr int kScanThreads = 1024;
 constexpr int kMaxRowFrames = 1024;
 
 struct RowFrames {
-  int32_t f0, f1;                  // segments touched by the row's query blocks
+  int32_t f0, f1;                  // segments touched by the pair's query blocks
   int16_t lo[kMaxRowFrames];       // window of frame f0 + i
   int16_t hi[kMaxRowFrames];
 };
-
-// The query blocks of row r: r itself (CSR rows), or 2r and 2r+1 (pair rows;
-// the last pair of an odd nb has one block, qb1 == qb0).
-__device__ inline void row_blocks(bool pair, int32_t r, int32_t nb, int32_t* qb0,
-                                  int32_t* qb1) {
-  *qb0 = pair ? 2 * r : r;
-  *qb1 = pair ? imin(2 * r + 1, nb - 1) : r;
-}
 
 // tau in A(t) for segments t, tau (segment T = the text tokens, attended by
 // and attending to everything).
@@ -85,16 +79,17 @@ __device__ inline bool keeps(const FrameCfg& c, const RowFrames& rf, int32_t t0,
   return false;
 }
 
-// Per-row test: which of the row's query blocks keep key block kb.
+// Per-pair test: which of the pair's query blocks keep key block kb.
 struct RowTest {
-  int32_t qb0, qb1;          // query blocks (equal for a CSR row)
+  int32_t qb0, qb1;          // 2p and 2p+1 (equal for the last pair of an odd nb)
   int32_t a0, a1, b0, b1;    // segments touched by qb0 and by qb1
 };
 
-__device__ inline RowTest row_test(const FrameCfg& c, bool pair, int32_t r, int32_t P,
-                                   int32_t B, int32_t N, int32_t nb) {
+__device__ inline RowTest row_test(const FrameCfg& c, int32_t p, int32_t P, int32_t B,
+                                   int32_t N, int32_t nb) {
   RowTest rt;
-  row_blocks(pair, r, nb, &rt.qb0, &rt.qb1);
+  rt.qb0 = 2 * p;
+  rt.qb1 = imin(2 * p + 1, nb - 1);
   block_frame_range(rt.qb0, c.T, P, B, N, &rt.a0, &rt.a1);
   block_frame_range(rt.qb1, c.T, P, B, N, &rt.b0, &rt.b1);
   return rt;
@@ -107,31 +102,47 @@ __device__ inline void kept_by(const FrameCfg& c, const RowFrames& rf, const Row
   *k1 = rt.qb1 != rt.qb0 && keeps(c, rf, rt.b0, rt.b1, kb, P, B, N);
 }
 
-template <bool PAIR>
+// Sums of three per-thread counts over the workgroup (thread 0's result).
+__device__ inline void block_sum3(int32_t (&v)[3], int32_t (*s_cnt)[kRowWaves]) {
+  for (int i = 0; i < 3; ++i) {
+    for (int off = 32; off > 0; off >>= 1) v[i] += __shfl_xor(v[i], off);
+    if (threadIdx.x % 64 == 0) s_cnt[i][threadIdx.x / 64] = v[i];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0)
+    for (int i = 0; i < 3; ++i) {
+      v[i] = 0;
+      for (int w = 0; w < kRowWaves; ++w) v[i] += s_cnt[i][w];
+    }
+}
+
 __global__ __launch_bounds__(kRowThreads) void count_rows_kernel(
-    FrameCfg c, int32_t P, int32_t B, int32_t* __restrict__ row_ptr) {
+    FrameCfg c, int32_t P, int32_t B, int32_t* __restrict__ row_ptr,
+    int32_t* __restrict__ pair_ptr) {
   __shared__ RowFrames rf;
-  __shared__ int32_t s_cnt[kRowWaves];
+  __shared__ int32_t s_cnt[3][kRowWaves];
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
-  const int32_t r = blockIdx.x;
-  const RowTest rt = row_test(c, PAIR, r, P, B, N, nb);
+  const int32_t p = blockIdx.x;
+  const RowTest rt = row_test(c, p, P, B, N, nb);
   load_row_frames(c, rt.qb0, rt.qb1, P, B, N, &rf);
-  int32_t cnt = 0;
+  int32_t cnt[3] = {0, 0, 0};   // row qb0, row qb1, pair row
   for (int32_t kb = threadIdx.x; kb < nb; kb += kRowThreads) {
     bool k0, k1;
     kept_by(c, rf, rt, kb, P, B, N, &k0, &k1);
-    cnt += (k0 || k1) ? 1 : 0;
+    cnt[0] += k0 ? 1 : 0;
+    cnt[1] += k1 ? 1 : 0;
+    cnt[2] += (k0 || k1) ? 1 : 0;
   }
-  // wave sums, then the workgroup sum
-  for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
-  if (threadIdx.x % 64 == 0) s_cnt[threadIdx.x / 64] = cnt;
-  __syncthreads();
+  block_sum3(cnt, s_cnt);
   if (threadIdx.x == 0) {
-    int32_t total = 0;
-    for (int w = 0; w < kRowWaves; ++w) total += s_cnt[w];
-    row_ptr[r + 1] = total;
-    if (r == 0) row_ptr[0] = 0;
+    row_ptr[rt.qb0 + 1] = cnt[0];
+    if (rt.qb1 != rt.qb0) row_ptr[rt.qb1 + 1] = cnt[1];
+    pair_ptr[p + 1] = cnt[2];
+    if (p == 0) {
+      row_ptr[0] = 0;
+      pair_ptr[0] = 0;
+    }
   }
 }
 
@@ -160,50 +171,56 @@ __global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(int32_t rows,
   }
 }
 
-// CSR rows: col_idx and/or entry words (either may be null).  Pair rows:
-// pair words into `words`, in the token-exact form when `exact`.
-template <bool PAIR>
+// The CSR rows of the pair's query blocks (col_idx and/or entry words,
+// either may be null) and the pair row (pair words, in the token-exact form
+// when `exact`).
 __global__ __launch_bounds__(kRowThreads) void fill_rows_kernel(
     FrameCfg c, int32_t P, int32_t B, const int32_t* __restrict__ row_ptr,
-    int32_t* __restrict__ col_idx, uint32_t* __restrict__ words, bool exact) {
+    int32_t* __restrict__ col_idx, uint32_t* __restrict__ entry,
+    const int32_t* __restrict__ pair_ptr, uint32_t* __restrict__ pair_words, bool exact) {
   __shared__ RowFrames rf;
-  __shared__ int32_t s_wave[kRowWaves];
+  __shared__ int32_t s_wave[3][kRowWaves];
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
-  const int32_t r = blockIdx.x;
-  const RowTest rt = row_test(c, PAIR, r, P, B, N, nb);
+  const int32_t p = blockIdx.x;
+  const RowTest rt = row_test(c, p, P, B, N, nb);
   load_row_frames(c, rt.qb0, rt.qb1, P, B, N, &rf);
   const int32_t lane = threadIdx.x % 64, wave = threadIdx.x / 64;
-  int32_t pos = row_ptr[r];
+  int32_t pos[3] = {row_ptr[rt.qb0], row_ptr[rt.qb1], pair_ptr[p]};
   auto attends = [&](int32_t t, int32_t tau) { return seg_attends(c, rf, t, tau); };
   for (int32_t base = 0; base < nb; base += kRowThreads) {
     const int32_t kb = base + (int32_t)threadIdx.x;
     bool k0 = false, k1 = false;
     if (kb < nb) kept_by(c, rf, rt, kb, P, B, N, &k0, &k1);
-    const bool keep = k0 || k1;
-    const uint64_t bal = __ballot(keep);
-    const int32_t below = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) s_wave[wave] = __popcll(bal);
+    const bool keep[3] = {k0, k1, k0 || k1};
+    int32_t at[3];
+    for (int i = 0; i < 3; ++i) {
+      const uint64_t bal = __ballot(keep[i]);
+      at[i] = __popcll(bal & ((1ull << lane) - 1ull));
+      if (lane == 0) s_wave[i][wave] = __popcll(bal);
+    }
     __syncthreads();
-    int32_t off = 0, total = 0;
-    for (int w = 0; w < kRowWaves; ++w) {
-      off += w < wave ? s_wave[w] : 0;
-      total += s_wave[w];
-    }
-    if (keep) {
-      const int32_t at = pos + off + below;
-      if (!PAIR) {
-        if (col_idx) col_idx[at] = kb;
-        if (words) words[at] = exact_entry(kb, rt.a0, rt.a1, c.T, P, B, N, attends);
-      } else if (exact) {
-        const uint32_t e0 = k0 ? exact_entry(kb, rt.a0, rt.a1, c.T, P, B, N, attends) : 0u;
-        const uint32_t e1 = k1 ? exact_entry(kb, rt.b0, rt.b1, c.T, P, B, N, attends) : 0u;
-        words[at] = pair_exact_word(e0, e1);
-      } else {
-        words[at] = pair_word_of(kb, k0, k1);
+    for (int i = 0; i < 3; ++i) {
+      int32_t off = 0, total = 0;
+      for (int w = 0; w < kRowWaves; ++w) {
+        off += w < wave ? s_wave[i][w] : 0;
+        total += s_wave[i][w];
       }
+      at[i] += pos[i] + off;
+      pos[i] += total;
     }
-    pos += total;
+    uint32_t e0 = 0u, e1 = 0u;
+    if (k0 && (entry || exact)) e0 = exact_entry(kb, rt.a0, rt.a1, c.T, P, B, N, attends);
+    if (k1 && (entry || exact)) e1 = exact_entry(kb, rt.b0, rt.b1, c.T, P, B, N, attends);
+    if (k0) {
+      if (col_idx) col_idx[at[0]] = kb;
+      if (entry) entry[at[0]] = e0;
+    }
+    if (k1) {
+      if (col_idx) col_idx[at[1]] = kb;
+      if (entry) entry[at[1]] = e1;
+    }
+    if (k0 || k1) pair_words[at[2]] = exact ? pair_exact_word(e0, e1) : pair_word_of(kb, k0, k1);
     __syncthreads();
   }
 }
@@ -222,17 +239,13 @@ hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     hipStream_t stream) {
   const int32_t nb = (int32_t)((mask_tokens(c, P) + B - 1) / B);
   const int32_t npairs = (nb + 1) / 2;
-  hipLaunchKernelGGL(count_rows_kernel<false>, dim3(nb), dim3(kRowThreads), 0, stream, c, P,
-                     B, d_row_ptr);
+  hipLaunchKernelGGL(count_rows_kernel, dim3(npairs), dim3(kRowThreads), 0, stream, c, P, B,
+                     d_row_ptr, d_pair_ptr);
   hipLaunchKernelGGL(scan_rows_kernel, dim3(1), dim3(kScanThreads), 0, stream, nb, d_row_ptr);
-  hipLaunchKernelGGL(fill_rows_kernel<false>, dim3(nb), dim3(kRowThreads), 0, stream, c, P, B,
-                     d_row_ptr, d_col_idx, d_entry, false);
-  hipLaunchKernelGGL(count_rows_kernel<true>, dim3(npairs), dim3(kRowThreads), 0, stream, c,
-                     P, B, d_pair_ptr);
   hipLaunchKernelGGL(scan_rows_kernel, dim3(1), dim3(kScanThreads), 0, stream, npairs,
                      d_pair_ptr);
-  hipLaunchKernelGGL(fill_rows_kernel<true>, dim3(npairs), dim3(kRowThreads), 0, stream, c, P,
-                     B, d_pair_ptr, nullptr, d_pair_word, exact);
+  hipLaunchKernelGGL(fill_rows_kernel, dim3(npairs), dim3(kRowThreads), 0, stream, c, P, B,
+                     d_row_ptr, d_col_idx, d_entry, d_pair_ptr, d_pair_word, exact);
   return hipGetLastError();
 }
 

@@ -114,7 +114,10 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
 }
 
 // Pair schedule: rows 2p and 2p+1 of the CSR merged (both ascending, no
-// repeats), each key block tagged with the rows that hold it.
+// repeats), each key block tagged with the rows that hold it.  Two passes
+// (row lengths, then the words into arrays of the final size); rows that are
+// equal, the common case (the two query blocks touch the same frames), are
+// copied with both tags instead of merged.
 void build_pairs_host(const std::vector<int32_t>& row_ptr,
                       const std::vector<int32_t>& col_idx,
                       const std::vector<uint32_t>* entry,
@@ -124,28 +127,65 @@ void build_pairs_host(const std::vector<int32_t>& row_ptr,
   const int32_t nb = (int32_t)row_ptr.size() - 1;
   const int32_t npairs = (nb + 1) / 2;
   const bool exact = entry != nullptr && pair_exact != nullptr;
+  const int32_t* ci = col_idx.data();
+  // Rows of pair p: [i0, i1) and [k0, k1) (empty for the second row of an
+  // odd nb's last pair).
+  auto rows = [&](int32_t p, int64_t* i0, int64_t* i1, int64_t* k0, int64_t* k1) {
+    *i0 = row_ptr[2 * p];
+    *i1 = row_ptr[2 * p + 1];
+    *k0 = 2 * p + 1 < nb ? row_ptr[2 * p + 1] : 0;
+    *k1 = 2 * p + 1 < nb ? row_ptr[2 * p + 2] : 0;
+  };
+  auto same = [&](int64_t i0, int64_t i1, int64_t k0, int64_t k1) {
+    return k1 - k0 == i1 - i0 &&
+           std::memcmp(ci + i0, ci + k0, sizeof(int32_t) * (size_t)(i1 - i0)) == 0;
+  };
+  // Pass 1: row lengths.
   pair_ptr->assign(npairs + 1, 0);
-  pair_word->clear();
-  if (exact) pair_exact->clear();
-  pair_word->reserve(col_idx.size());
-  if (exact) pair_exact->reserve(col_idx.size());
   for (int32_t p = 0; p < npairs; ++p) {
-    int64_t i = row_ptr[2 * p];
-    const int64_t ie = row_ptr[2 * p + 1];
-    int64_t k = 2 * p + 1 < nb ? row_ptr[2 * p + 1] : 0;
-    const int64_t ke = 2 * p + 1 < nb ? row_ptr[2 * p + 2] : 0;
+    int64_t i, ie, k, ke;
+    rows(p, &i, &ie, &k, &ke);
+    int64_t len = 0;
+    if (same(i, ie, k, ke)) {
+      len = ie - i;
+    } else {
+      while (i < ie && k < ke) {
+        const int32_t x = ci[i], y = ci[k];
+        i += x <= y;
+        k += y <= x;
+        ++len;
+      }
+      len += (ie - i) + (ke - k);
+    }
+    (*pair_ptr)[p + 1] = (*pair_ptr)[p] + (int32_t)len;
+  }
+  // Pass 2: the words.
+  pair_word->resize((size_t)(*pair_ptr)[npairs]);
+  if (exact) pair_exact->resize(pair_word->size());
+  uint32_t* w = pair_word->data();
+  uint32_t* we = exact ? pair_exact->data() : nullptr;
+  const uint32_t* en = exact ? entry->data() : nullptr;
+  for (int32_t p = 0; p < npairs; ++p) {
+    int64_t i, ie, k, ke;
+    rows(p, &i, &ie, &k, &ke);
+    int64_t o = (*pair_ptr)[p];
+    if (same(i, ie, k, ke)) {
+      for (int64_t n = 0; n < ie - i; ++n) w[o + n] = pair_word_of(ci[i + n], true, true);
+      if (exact)
+        for (int64_t n = 0; n < ie - i; ++n) we[o + n] = pair_exact_word(en[i + n], en[k + n]);
+      continue;
+    }
     while (i < ie || k < ke) {
-      const int32_t x = i < ie ? col_idx[i] : INT32_MAX;
-      const int32_t y = k < ke ? col_idx[k] : INT32_MAX;
+      const int32_t x = i < ie ? ci[i] : INT32_MAX;
+      const int32_t y = k < ke ? ci[k] : INT32_MAX;
       const int32_t kb = x < y ? x : y;
       const bool in0 = x == kb, in1 = y == kb;
-      pair_word->push_back(pair_word_of(kb, in0, in1));
-      if (exact)
-        pair_exact->push_back(pair_exact_word(in0 ? (*entry)[i] : 0u, in1 ? (*entry)[k] : 0u));
+      w[o] = pair_word_of(kb, in0, in1);
+      if (exact) we[o] = pair_exact_word(in0 ? en[i] : 0u, in1 ? en[k] : 0u);
+      ++o;
       if (in0) ++i;
       if (in1) ++k;
     }
-    (*pair_ptr)[p + 1] = (int32_t)pair_word->size();
   }
 }
 
