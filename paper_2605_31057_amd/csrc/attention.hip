@@ -1,8 +1,9 @@
 // attention.hip -- block-sparse and dense flash-attention forward for gfx950.
 //
 // Computes Eq. 2 of the LVSA paper (softmax attention restricted to a key
-// set) with the key set of every query block given by a block CSR, and Eq. 1
-// (all keys) with the same kernel visiting every key block.
+// set) with the key set of every query block given by a block mask (read in
+// its pair-schedule form), and Eq. 1 (all keys) with the same kernel visiting
+// every key block.
 //
 // Work decomposition
 //   One workgroup per (head, pair of query blocks 2p and 2p+1): 2*BLOCK query
@@ -88,9 +89,10 @@ __device__ __forceinline__ float pair_max(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// LDS tile layout ("slabs").  A BLOCK x 128 tile is stored as 4 slabs of 32
-// columns; a slab row is 64 bytes (4 chunks of 16 bytes) and rows follow each
-// other, so tile byte (slab, row, chunk) = slab*BLOCK*64 + row*64 + chunk*16.
+// LDS tile layout ("slabs").  A KEYS x 128 tile (one step's keys) is stored
+// as 4 slabs of 32 columns; a slab row is 64 bytes (4 chunks of 16 bytes) and
+// rows follow each other, so tile byte (slab, row, chunk) =
+// slab*KEYS*64 + row*64 + chunk*16.
 // The chunk is XORed with x(row) = (row/4) % 4.  With 64 banks of 4 bytes:
 //   - ds_read_b128 (served 16 lanes at a time) reads 16 consecutive rows at
 //     one logical chunk: 4 rows share a bank window and the XOR separates them;
@@ -113,14 +115,14 @@ struct Tile {
   static constexpr int NT = NW * 64;                // threads
   static constexpr int KTW = KEYS / 32;             // 32-key tiles per step
   static constexpr int SLAB = KEYS * SLAB_ROW;      // bytes per slab
-  static constexpr int BYTES = 4 * SLAB;        // bytes per tile
-  static constexpr int INSTR = BYTES / 1024;    // 1 KiB wave loads per tile
-  static constexpr int LOADS = INSTR / NW;      // per wave per tile
-  static constexpr int IPS = SLAB / 1024;       // wave loads per slab
+  static constexpr int BYTES = 4 * SLAB;            // bytes per tile
+  static constexpr int INSTR = BYTES / 1024;        // 1 KiB wave loads per tile
+  static constexpr int LOADS = INSTR / NW;          // per wave per tile
+  static constexpr int IPS = SLAB / 1024;           // wave loads per slab
   static_assert(LOADS * NW == INSTR, "tile load mapping");
 };
 
-// Issues the direct-to-LDS loads of rows kb*BLOCK .. +BLOCK-1 of one tensor
+// Issues the direct-to-LDS loads of the KEYS rows of one step of one tensor
 // into the tile at LDS byte address `lds`.  Wave load I fills tile bytes
 // 1024*I .. +1023: slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk
 // lane%4, which holds logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).
