@@ -235,3 +235,37 @@ def test_large_logits_exercise_the_rescale(scale):
     dref = OA.dense_attention(qf, kf, vf)
     err = np.abs(dense.float().cpu().numpy() - dref)
     assert_close(float(err.max()), float(err.mean()))
+
+
+@pytest.mark.parametrize("T,P,B,exact", [(9, 150, 64, False), (9, 150, 64, True),
+                                         (12, 200, 128, False), (12, 200, 128, True)])
+def test_pairs_whose_rows_differ(T, P, B, exact):
+    """The kernel walks query blocks in pairs over the union of their key
+    lists; where a frame edge falls between the two blocks their rows differ
+    and each block's waves must drop the other's extra key blocks.  Shapes
+    where that happens in most pairs (narrow windows, P not a multiple of B),
+    both forms, against the oracle over every row."""
+    H, W, tper = 2, 0, 5
+    N = T * P
+    p = L.Params(window=W, tper=tper)
+    _say(f"[pairs] T={T} P={P} B={B} exact={exact}")
+    csr = L.build_mask(T, P, B, 2, p, exact=exact)
+    rp, ci = csr.arrays()
+    ptr, words, _ = csr.pairs()
+    split = sum(1 for w in words.tolist() if (w >> 30) != 3)
+    assert split > len(words) // 10, (split, len(words))   # the case is exercised
+    q, k, v = make_qkv(H, N, seed=T * 10 + B)
+    qd, kd, vd = (x.cuda() for x in (q, k, v))
+    csr.upload()
+    qf, kf, vf = (x.float().numpy() for x in (q, k, v))
+    if exact:
+        out = L.attention_exact(qd, kd, vd, csr.exact_mask())
+        _, _, A = M.attended_frames(T, 2, W=W, tper=tper)
+        ref = OA.frame_sparse_attention(qf, kf, vf, A, P)
+    else:
+        out = L.attention(qd, kd, vd, csr.device_mask())
+        ref = OA.assemble(OA.block_sparse_attention(qf, kf, vf, rp.tolist(), ci.tolist(), B),
+                          H, N, 128, B)
+    torch.cuda.synchronize()
+    err = np.abs(out.float().cpu().numpy() - ref)
+    assert_close(float(err.max()), float(err.mean()))
