@@ -13,7 +13,8 @@
  * The library has two halves:
  *   - mask builders that turn (T, P, block, step, params) into per-query-block
  *     lists of kept key blocks (a block CSR), on the host (lvsa_build_mask)
- *     or on the device (lvsa_build_mask_device);
+ *     or on the device (lvsa_build_mask_device), together with the same mask
+ *     arranged per pair of query blocks (the pair schedule the kernel reads);
  *   - a block-sparse flash-attention forward pass that visits only the kept
  *     blocks (lvsa_attention), and a dense pass of the same design over every
  *     block (lvsa_dense_attention, Eq. 1) used as the speed baseline.
