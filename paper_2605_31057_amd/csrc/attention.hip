@@ -11,13 +11,13 @@
 //   0..NW/2-1 hold rows of query block 2p, the others rows of 2p+1.  The
 //   workgroup walks the pair's schedule (the union of the two blocks' key
 //   lists, each word saying which of the two keeps the key block, lvsa.h) one
-//   half key block (KEYS = BLOCK/2 keys) per step, and every wave takes all
-//   KEYS keys of the step for its rows.  Adjacent query blocks mostly keep the
-//   same key blocks (they touch the same frames), so each K/V tile brought
-//   from HBM/L2 into LDS serves 2*BLOCK query rows; a key block that only one
-//   of the two keeps is masked out (no valid keys) for the other's waves.
+//   key block per step, and every wave takes all BLOCK keys of the step for
+//   its rows.  Adjacent query blocks mostly keep the same key blocks (they
+//   touch the same frames), so each K/V tile brought from HBM/L2 into LDS
+//   serves 2*BLOCK query rows; a key block that only one of the two keeps is
+//   masked out (no valid keys) for the other's waves.
 //
-// Schedule ("ping-pong", one half key block per step)
+// Schedule ("ping-pong", one key block per step)
 //   Waves w and w + NW/2 (which share a SIMD when NW = 8) run half a step
 //   apart: while one is in its GEMM phase (O += P(j) V(j), l += row sums of
 //   P(j), S(j+1) = K(j+1) Q^T: MFMA with fragments from LDS) the other is in
@@ -30,9 +30,14 @@
 //   size bound turns rows at or past N (ragged last block) into zeros.
 //   Row sums come from the matrix core: in the GEMM phase a 16x16x32 MFMA
 //   with a constant 0/1 A operand adds up each 16-key step of P for all 32
-//   rows of the wave.  That takes 32 adds per step off the softmax phase, for
-//   4 small MFMAs (1/16 of the step's matrix work), and sums exactly the bf16
-//   P that multiplies V.
+//   rows of the wave.  That takes the adds off the softmax phase, for 8 small
+//   MFMAs per step (1/16 of the step's matrix work), and sums exactly the
+//   bf16 P that multiplies V.
+//   A whole key block per step keeps the per-step costs (two barriers, the
+//   loop, the load set-up) small against the step's 72 MFMAs per wave; S
+//   (64 registers) and P (32) then fill the register file, so the GEMM
+//   phase finishes P(j) before it produces S(j+1) and the masks avoid
+//   per-element lane masks (comparisons into SGPR pairs).
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
@@ -89,10 +94,10 @@ __device__ __forceinline__ float pair_max(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// LDS tile layout ("slabs").  A KEYS x 128 tile (one step's keys) is stored
+// LDS tile layout ("slabs").  A BLOCK x 128 tile (one key block) is stored
 // as 4 slabs of 32 columns; a slab row is 64 bytes (4 chunks of 16 bytes) and
 // rows follow each other, so tile byte (slab, row, chunk) =
-// slab*KEYS*64 + row*64 + chunk*16.
+// slab*BLOCK*64 + row*64 + chunk*16.
 // The chunk is XORed with x(row) = (row/4) % 4.  With 64 banks of 4 bytes:
 //   - ds_read_b128 (served 16 lanes at a time) reads 16 consecutive rows at
 //     one logical chunk: 4 rows share a bank window and the XOR separates them;
@@ -110,11 +115,10 @@ constexpr int QT = LVSA_QT;   // 32-row query tiles per wave
 
 template <int BLOCK>
 struct Tile {
-  static constexpr int KEYS = BLOCK / 2;            // keys per pipeline step
   static constexpr int NW = 2 * BLOCK / (32 * QT);  // waves (32*QT query rows each)
   static constexpr int NT = NW * 64;                // threads
-  static constexpr int KTW = KEYS / 32;             // 32-key tiles per step
-  static constexpr int SLAB = KEYS * SLAB_ROW;      // bytes per slab
+  static constexpr int KTW = BLOCK / 32;            // 32-key tiles per step
+  static constexpr int SLAB = BLOCK * SLAB_ROW;     // bytes per slab
   static constexpr int BYTES = 4 * SLAB;            // bytes per tile
   static constexpr int INSTR = BYTES / 1024;        // 1 KiB wave loads per tile
   static constexpr int LOADS = INSTR / NW;          // per wave per tile
@@ -122,7 +126,7 @@ struct Tile {
   static_assert(LOADS * NW == INSTR, "tile load mapping");
 };
 
-// Issues the direct-to-LDS loads of the KEYS rows of one step of one tensor
+// Issues the direct-to-LDS loads of rows kb*BLOCK .. +BLOCK-1 of one tensor
 // into the tile at LDS byte address `lds`.  Wave load I fills tile bytes
 // 1024*I .. +1023: slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk
 // lane%4, which holds logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).
@@ -147,17 +151,15 @@ __device__ __forceinline__ void issue_load(uint32_t lds_dst, __amdgpu_buffer_rsr
       : "memory", "m0");
 }
 
-// Buffer resource over rows sb*KEYS .. N-1 of one head of K or V (sub-block
-// sb = half sb%2 of key block sb/2); an index outside [0, nsb), nsb the
-// number of sub-blocks holding keys below N, yields an empty resource (all
-// loads read 0).
+// Buffer resource over rows kb*BLOCK .. N-1 of one head of K or V; a key
+// block index outside [0, nb) yields an empty resource (all loads read 0).
 template <int BLOCK>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const __bf16* head_base,
                                                             int64_t row_elems,
                                                             uint32_t head_bytes,
-                                                            int sb, int nsb) {
-  const bool ok = (uint32_t)sb < (uint32_t)nsb;
-  const int64_t skip = ok ? (int64_t)sb * Tile<BLOCK>::KEYS * row_elems : 0;
+                                                            int kb, int nb) {
+  const bool ok = (uint32_t)kb < (uint32_t)nb;
+  const int64_t skip = ok ? (int64_t)kb * BLOCK * row_elems : 0;
   const uint32_t bytes = ok ? head_bytes - (uint32_t)(skip * 2) : 0u;
   return make_rsrc(head_base + skip, bytes);
 }
@@ -167,27 +169,26 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const __bf16* head_b
 // logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).  The per-lane part
 // of the global offset is (lane/4)*row_bytes + 16*((lane%4) ^ (lane/16)); the
 // per-load part is uniform.
+// Per-wave load plan: wave w's load j of a tile fills tile bytes
+// 1024*(w + NW*j): slab j, rows 16*w + lane/4 (NW = IPS: one wave per 16-row
+// band of a slab), physical chunk lane%4, which holds logical chunk
+// (lane%4) ^ x(row) = (lane%4) ^ (lane/16).  Global offset: lane_off plus
+// 64*j; LDS offset: lds_w plus 1024*NW*j.
 template <int BLOCK>
 struct LoadPlan {
-  uint32_t lane_off;
-  uint32_t part[Tile<BLOCK>::LOADS];
-  uint32_t lds_part[Tile<BLOCK>::LOADS];
+  uint32_t lane_off;   // (16*w + lane/4)*row_bytes + 16*((lane%4) ^ (lane/16))
+  uint32_t lds_w;      // 1024*w (uniform)
 };
 
 template <int BLOCK>
 __device__ __forceinline__ LoadPlan<BLOCK> load_plan(uint32_t row_bytes, int wave,
                                                      int lane) {
   using TL = Tile<BLOCK>;
+  static_assert(TL::NW == TL::IPS, "one wave per 16-row band of a slab");
   LoadPlan<BLOCK> lp;
-  lp.lane_off = (uint32_t)(lane / 4) * row_bytes +
+  lp.lane_off = (uint32_t)(16 * wave + lane / 4) * row_bytes +
                 16u * (uint32_t)((lane % 4) ^ (lane / 16));
-#pragma unroll
-  for (int j = 0; j < TL::LOADS; ++j) {
-    const int I = wave + TL::NW * j;
-    lp.part[j] = (uint32_t)__builtin_amdgcn_readfirstlane(
-        16u * (uint32_t)(I % TL::IPS) * row_bytes + (uint32_t)(64 * (I / TL::IPS)));
-    lp.lds_part[j] = (uint32_t)__builtin_amdgcn_readfirstlane(1024u * (uint32_t)I);
-  }
+  lp.lds_w = (uint32_t)__builtin_amdgcn_readfirstlane(1024u * (uint32_t)wave);
   return lp;
 }
 
@@ -197,7 +198,7 @@ __device__ __forceinline__ void issue_tile(uint32_t lds, __amdgpu_buffer_rsrc_t 
   using TL = Tile<BLOCK>;
 #pragma unroll
   for (int j = 0; j < TL::LOADS; ++j)
-    issue_load(lds + lp.lds_part[j], rsrc, lp.lane_off + lp.part[j]);
+    issue_load(lds + lp.lds_w + 1024u * TL::NW * j, rsrc, lp.lane_off + 64u * j);
 }
 
 // The loads of one pipeline step: the next K tile and the next V tile, spread
@@ -216,10 +217,10 @@ template <int BLOCK>
 __device__ __forceinline__ void issue_step_load(const StepLoads<BLOCK>& sl, int i) {
   using TL = Tile<BLOCK>;
   if (i < TL::LOADS)
-    issue_load(sl.k_dst + sl.kp->lds_part[i], sl.rk, sl.kp->lane_off + sl.kp->part[i]);
+    issue_load(sl.k_dst + sl.kp->lds_w + 1024u * TL::NW * i, sl.rk, sl.kp->lane_off + 64u * i);
   else
-    issue_load(sl.v_dst + sl.vp->lds_part[i - TL::LOADS], sl.rv,
-               sl.vp->lane_off + sl.vp->part[i - TL::LOADS]);
+    issue_load(sl.v_dst + sl.vp->lds_w + 1024u * TL::NW * (i - TL::LOADS), sl.rv,
+               sl.vp->lane_off + 64u * (i - TL::LOADS));
 }
 
 __device__ __forceinline__ void wait_loads_and_sync() {
@@ -295,23 +296,24 @@ struct WaveState {
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
-// -inf.  `valid` = N - first key of the step (0 or less: no key is valid).
+// -inf.  `valid` = N - first key of the block (0: no key is valid).
 template <int BLOCK>
 __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
-  if (valid < TL::KEYS) {
-    // key = lane part + constant part; compare the constant part with a
-    // per-lane limit so no per-element key index is kept in a register.
-    const int lim = valid - 4 * hl;
+  if (valid < BLOCK) {
+    // key = lane part + constant part off: the key is valid iff
+    // valid - lane part - 1/2 - off > 0, so each score takes the min with
+    // +inf or -inf of that sign (no per-element comparisons into lane masks).
+    const float lim = (float)(valid - 4 * hl) - 0.5f;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int off = 32 * kt + 8 * (r / 4) + (r % 4);
-          if (off >= lim) sc.s[qt][kt][r] = -__builtin_inff();
+          const float off = (float)(32 * kt + 8 * (r / 4) + (r % 4));
+          sc.s[qt][kt][r] = fminf(sc.s[qt][kt][r], __builtin_copysignf(__builtin_inff(), lim - off));
         }
   }
 }
@@ -322,12 +324,11 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid
 // lies in the key block's second frame, which starts kfirst keys in; 0 = the
 // query block does not keep the key block).  A row's kept keys are then one
 // range [klo, khi) of the block, also clipped at `valid` = N minus the
-// block's first key; the step holds keys key0 .. key0+KEYS-1 of the block.
-// Scores outside the range become -inf.  Blocks whose every part is attended
-// and that are not ragged skip the masking.
+// block's first key.  Scores outside the range become -inf.  Blocks whose
+// every part is attended and that are not ragged skip the masking.
 template <int BLOCK>
 __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t pat,
-                                           int kfirst, int valid, int key0,
+                                           int kfirst, int valid,
                                            const bool (&second)[QT]) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
@@ -337,13 +338,18 @@ __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t
       const uint32_t bits = second[qt] ? pat >> 2 : pat;
       const int klo = (bits & 1u) ? 0 : kfirst;
       const int khi = (bits & 2u) ? valid : min(kfirst, valid);
-      const uint32_t width = (uint32_t)max(khi - klo, 0);
+      // key = kbase + c: kept iff klo <= key < khi, i.e. both
+      // (kbase - klo + 1/2) + c and (khi - 1/2 - kbase) - c are positive;
+      // min with +-inf by the sign of the smaller (no lane masks).
+      const int kbase = 4 * hl;
+      const float lo = (float)(kbase - klo) + 0.5f, hi = (float)(khi - kbase) - 0.5f;
 #pragma unroll
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = key0 + 32 * kt + 8 * (r / 4) + 4 * hl + (r % 4);
-          if ((uint32_t)(key - klo) >= width) sc.s[qt][kt][r] = -__builtin_inff();
+          const float c = (float)(32 * kt + 8 * (r / 4) + (r % 4));
+          sc.s[qt][kt][r] = fminf(sc.s[qt][kt][r],
+                                  __builtin_copysignf(__builtin_inff(), fminf(lo + c, hi - c)));
         }
     }
   }
@@ -357,8 +363,10 @@ struct Probs {
 // Softmax phase of the ping-pong schedule: block j's scores (in `sc`) become
 // its probabilities P (bf16, in `pr`), with the running max and, when the
 // max is raised, the rescale of O and l done here so that the next GEMM phase
-// only multiplies (and adds P up into l).  `sl` (may be null) carries tile loads to issue
-// along the way.
+// only multiplies (and adds P up into l).  `sl` (may be null) carries tile
+// loads to issue along the way.  Scheduling barriers every 8 scores keep the
+// compiler from hoisting many exponentials at once (S, P, O and Q already
+// fill the register file).
 template <int BLOCK>
 __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState<BLOCK>& st,
                                               Probs<BLOCK>& pr, float scale_log2,
@@ -388,6 +396,7 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
     const float msub = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
 #pragma unroll
     for (int el = 0; el < NE; el += 2) {
+      if (el % 8 == 0) __builtin_amdgcn_sched_barrier(0);
       if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
       const float a = __builtin_amdgcn_exp2f(
           __builtin_fmaf(sc.s[t][el / 16][el % 16], scale_log2, -msub));
@@ -402,11 +411,10 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
     for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
 }
 
-// GEMM phase of the ping-pong schedule: S(j+1) = K(j+1) Q^T into `sc` and
-// O += P(j) V(j), one MFMA of each in turn (independent accumulators back to
-// back), l += the row sums of P(j) (one 16x16x32 MFMA per 16-key step, `ones`
-// its A operand), with K and V fragments read AHEAD MFMAs early and the tile
-// loads in `sl` (may be null) spread over the phase.
+// GEMM phase of the ping-pong schedule: O += P(j) V(j) and l += the row sums
+// of P(j) (one 16x16x32 MFMA per 16-key step, `ones` its A operand), then
+// S(j+1) = K(j+1) Q^T into `sc`, with K and V fragments read AHEAD MFMAs
+// early and the tile loads in `sl` (may be null) spread over the phase.
 template <int BLOCK>
 __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
                                            const bf16x8 (&qf)[QT][8], Scores<BLOCK>& sc,
@@ -419,18 +427,19 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
   constexpr int NF = NS + NP;
   constexpr int AHEAD = 3;
   constexpr int NLOADS = 2 * TL::LOADS;
-  // Fragment i < NS: K, key tile i/8, d-step i%8.  Fragment NS + f: V^T,
-  // d tile f/(2*KTW), key tile (f/2)%KTW, k-step half f%2 -- so MFMAs on one
-  // accumulator follow each other.
+  // Fragment i < NP: V^T, d tile i/(2*KTW), key tile (i/2)%KTW, k-step half
+  // i%2.  Fragment NP + f: K, key tile f/8, d-step f%8.  MFMAs on one
+  // accumulator follow each other, and P(j) (with its row sums) is done
+  // before S(j+1) is produced, so the two are never live together.
   auto frag = [&](int i) -> bf16x8 {
-    if (i < NS) {
-      const int kt = i / 8, stp = i % 8;
+    if (i >= NP) {
+      const int f = i - NP;
+      const int kt = f / 8, stp = f % 8;
       const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) + (stp / 2) * TL::SLAB +
                            kt * 32 * SLAB_ROW;
       return *(const bf16x8*)(lds_k + off);
     }
-    const int f = i - NS;
-    const int dt = f / (2 * TL::KTW), kt = (f / 2) % TL::KTW, c = f % 2;
+    const int dt = i / (2 * TL::KTW), kt = (i / 2) % TL::KTW, c = i % 2;
     const uint32_t off = dt * TL::SLAB + (32 * kt + 16 * c) * SLAB_ROW;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_lo + off));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds_v + fa.v_hi + off));
@@ -444,30 +453,31 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
   for (int i = 0; i < NF; ++i) {
     if (i + AHEAD < NF) fr[i + AHEAD] = frag(i + AHEAD);
     if (sl && i % (NF / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NF / NLOADS));
-    if (i < NS) {
-      const int kt = i / 8, stp = i % 8;
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-        sc.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            fr[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
-    } else {
-      const int f = i - NS;
-      const int dt = f / (2 * TL::KTW), kt = (f / 2) % TL::KTW, c = f % 2;
+    if (i < NP) {
+      const int dt = i / (2 * TL::KTW), kt = (i / 2) % TL::KTW, c = i % 2;
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
         st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], pr.p[qt][kt][c],
                                                                st.o[qt][dt], 0, 0, 0);
+      if (i == NP - 1)
+#pragma unroll
+        for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt)
+              st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt2][c2],
+                                                                 st.l[qt], 0, 0, 0);
+    } else {
+      const int f = i - NP;
+      const int kt = f / 8, stp = f % 8;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+        sc.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            fr[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-#pragma unroll
-  for (int kt = 0; kt < TL::KTW; ++kt)
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-        st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt][c], st.l[qt],
-                                                           0, 0, 0);
 }
 
 // MODE: ATTN_DENSE (every key block), ATTN_BLOCK (block schedule words),
@@ -512,16 +522,15 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
   const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
   // Schedule words: key block in bits 0..29 (block form) or 0..15 (exact
-  // form); step j takes half j%2 of the j/2-th word's key block.
+  // form); step j takes the j-th word's key block.
   auto kb_of = [&](uint32_t w) {
     return (int)(EXACT ? (w & 0xFFFFu) : (w & 0x3FFFFFFFu));
   };
-  const int nsb = (N + TL::KEYS - 1) / TL::KEYS;   // sub-blocks holding keys < N
-  auto rk_at = [&](uint32_t w, int half) {
-    return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, 2 * kb_of(w) + half, nsb);
+  auto rk_at = [&](uint32_t w) {
+    return tile_rsrc<BLOCK>(kh_base, k_st, k_bytes, kb_of(w), nb);
   };
-  auto rv_at = [&](uint32_t w, int half) {
-    return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, 2 * kb_of(w) + half, nsb);
+  auto rv_at = [&](uint32_t w) {
+    return tile_rsrc<BLOCK>(vh_base, v_st, v_bytes, kb_of(w), nb);
   };
   const FragAddr fa = frag_addr(lane);
 
@@ -549,27 +558,26 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) second[qt] = rows0 + 32 * qt + li >= qfirst;
   }
-  // Masks the scores of step `half` of schedule word w for this wave's query
-  // block: a key block that block does not keep has no valid keys.
+  // Masks the scores of the key block of schedule word w for this wave's
+  // query block: a key block that block does not keep has no valid keys.
   const uint32_t kept_bit = upper ? 31u : 30u;       // block form
   const uint32_t pat_shift = upper ? 28u : 24u;      // exact form
-  auto mask_block = [&](Scores<BLOCK>& sc, uint32_t w, int half) {
+  auto mask_block = [&](Scores<BLOCK>& sc, uint32_t w) {
     const int kb = kb_of(w);
     if constexpr (EXACT)
       mask_exact<BLOCK>(sc, lane, (w >> pat_shift) & 0xFu, (int)((w >> 16) & 0xFFu),
-                        N - kb * BLOCK, TL::KEYS * half, second);
+                        N - kb * BLOCK, second);
     else
-      mask_tail<BLOCK>(sc, lane,
-                       ((w >> kept_bit) & 1u) ? N - (2 * kb + half) * TL::KEYS : 0);
+      mask_tail<BLOCK>(sc, lane, ((w >> kept_bit) & 1u) ? N - kb * BLOCK : 0);
   };
 
-  int beg = 0, n = 2 * nb;
+  int beg = 0, n = nb;
   if constexpr (SPARSE) {
     beg = sched_ptr[pq];
-    n = 2 * (sched_ptr[pq + 1] - beg);
+    n = sched_ptr[pq + 1] - beg;
   }
   auto word_at = [&](int j) -> uint32_t {   // schedule word of step j
-    return SPARSE ? sched[beg + j / 2] : ((uint32_t)(j / 2) | 0xC0000000u);
+    return SPARSE ? sched[beg + j] : ((uint32_t)j | 0xC0000000u);
   };
   // The word of step j+3 is fetched by a vector load one step before it is
   // needed, so the load's latency hides under a whole step (a scalar load
@@ -578,8 +586,8 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
       make_rsrc(sched, SPARSE ? (uint32_t)(sched_ptr[npairs] * 4) : 0u);
   auto word_fetch = [&](int j) -> uint32_t {   // VGPR value, clamped to the row
     const int jj = j < n ? j : n - 1;
-    if constexpr (!SPARSE) return (uint32_t)(jj / 2) | 0xC0000000u;
-    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsched, (beg + jj / 2) * 4, 0, 0);
+    if constexpr (!SPARSE) return (uint32_t)jj | 0xC0000000u;
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsched, (beg + jj) * 4, 0, 0);
   };
 
   WaveState<BLOCK> ws;
@@ -620,29 +628,28 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     const uint32_t w0 = word_at(0);
     uint32_t w1 = n > 1 ? word_at(1) : w0;     // step j+1
     uint32_t w2 = n > 2 ? word_at(2) : w1;     // step j+2
-    issue_tile<BLOCK>(k_slot0, rk_at(w0, 0), kp);
-    issue_tile<BLOCK>(v_slot0, rv_at(w0, 0), vp);
-    issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(w1, 1), kp);
+    issue_tile<BLOCK>(k_slot0, rk_at(w0), kp);
+    issue_tile<BLOCK>(v_slot0, rv_at(w0), vp);
+    issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(w1), kp);
     wait_loads_and_sync();
     Scores<BLOCK> sc;
     compute_scores<BLOCK>(k_lds, qf, sc, fa);   // S(0)
-    mask_block(sc, w0, 0);
+    mask_block(sc, w0);
     Probs<BLOCK> pr;
     if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
     __syncthreads();
     for (int j = 0; j < n; ++j) {
       const uint32_t w3v = word_fetch(j + 3);
-      const int h1 = (j + 1) & 1, h2 = j & 1;    // halves of steps j+1, j+2
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
-          rk_at(w2, h2), rv_at(w1, h1), &kp, &vp};
+          rk_at(w2), rv_at(w1), &kp, &vp};
       const char* const kj1 = k_lds + ((j + 1) & 1) * TL::BYTES;   // K(j+1)
       const char* const vj = v_lds + (j & 1) * TL::BYTES;          // V(j)
       // half-period 2j
       if (lead) {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, &sl);
-        mask_block(sc, w1, h1);
+        mask_block(sc, w1);
       } else {
         softmax_phase<BLOCK>(sc, ws, pr, scale_log2, &sl);
       }
@@ -652,7 +659,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
         if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
       } else {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
-        mask_block(sc, w1, h1);
+        mask_block(sc, w1);
       }
       wait_loads_and_sync();
       w1 = w2;
