@@ -296,24 +296,24 @@ struct WaveState {
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
-// -inf.  `valid` = N - first key of the block (0: no key is valid).
+// -inf.  `valid` = N - first key of the block (0: no key is valid).  Per
+// score one compare of a constant into VCC and one select, a scheduling
+// barrier every 4 scores so that few compare results are live at once.
 template <int BLOCK>
 __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid) {
   using TL = Tile<BLOCK>;
   const int hl = lane / 32;
   if (valid < BLOCK) {
-    // key = lane part + constant part off: the key is valid iff
-    // valid - lane part - 1/2 - off > 0, so each score takes the min with
-    // +inf or -inf of that sign (no per-element comparisons into lane masks).
-    const float lim = (float)(valid - 4 * hl) - 0.5f;
+    const int lim = valid - 4 * hl;   // key 4*hl + c is valid iff c < lim
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float off = (float)(32 * kt + 8 * (r / 4) + (r % 4));
-          sc.s[qt][kt][r] = fminf(sc.s[qt][kt][r], __builtin_copysignf(__builtin_inff(), lim - off));
+          if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+          const int c = 32 * kt + 8 * (r / 4) + (r % 4);
+          sc.s[qt][kt][r] = c < lim ? sc.s[qt][kt][r] : -__builtin_inff();
         }
   }
 }
@@ -326,6 +326,11 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid
 // range [klo, khi) of the block, also clipped at `valid` = N minus the
 // block's first key.  Scores outside the range become -inf.  Blocks whose
 // every part is attended and that are not ragged skip the masking.
+//
+// Key kbase + c is kept iff the unsigned c + kbase - klo is below the range's
+// width: per score one add of a constant, one compare into VCC and one
+// select.  A scheduling barrier every 4 scores keeps the compiler from
+// computing many compare results ahead (each holds an SGPR pair).
 template <int BLOCK>
 __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t pat,
                                            int kfirst, int valid,
@@ -338,18 +343,15 @@ __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t
       const uint32_t bits = second[qt] ? pat >> 2 : pat;
       const int klo = (bits & 1u) ? 0 : kfirst;
       const int khi = (bits & 2u) ? valid : min(kfirst, valid);
-      // key = kbase + c: kept iff klo <= key < khi, i.e. both
-      // (kbase - klo + 1/2) + c and (khi - 1/2 - kbase) - c are positive;
-      // min with +-inf by the sign of the smaller (no lane masks).
-      const int kbase = 4 * hl;
-      const float lo = (float)(kbase - klo) + 0.5f, hi = (float)(khi - kbase) - 0.5f;
+      const uint32_t shift = (uint32_t)(4 * hl - klo);
+      const uint32_t width = (uint32_t)max(khi - klo, 0);
 #pragma unroll
       for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float c = (float)(32 * kt + 8 * (r / 4) + (r % 4));
-          sc.s[qt][kt][r] = fminf(sc.s[qt][kt][r],
-                                  __builtin_copysignf(__builtin_inff(), fminf(lo + c, hi - c)));
+          if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+          const uint32_t c = (uint32_t)(32 * kt + 8 * (r / 4) + (r % 4));
+          sc.s[qt][kt][r] = c + shift < width ? sc.s[qt][kt][r] : -__builtin_inff();
         }
     }
   }
@@ -508,7 +510,12 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const int npairs = (nb + 1) / 2;
   const int tile = xcd_remap(blockIdx.x, npairs * H);
   const int head = tile / npairs;
-  const int pq = tile % npairs;                 // query blocks 2pq, 2pq+1
+  // Pairs of a head go last to first: rows that attend every key block (text
+  // tokens, placed after the video tokens) are the longest tiles, and taking
+  // them first keeps them out of the grid's tail (each row's key blocks are
+  // then walked in descending order, which keeps neighbouring workgroups'
+  // shared blocks in L2).
+  const int pq = npairs - 1 - tile % npairs;    // query blocks 2pq, 2pq+1
   const bool upper = wave >= TL::NW / 2;        // rows of query block 2pq+1
   const int qb = 2 * pq + (upper ? 1 : 0);
   const int rows0 = 32 * QT * (wave % (TL::NW / 2));   // first row within qb
@@ -522,7 +529,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
   const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
   // Schedule words: key block in bits 0..29 (block form) or 0..15 (exact
-  // form); step j takes the j-th word's key block.
+  // form); the words of a row are walked last to first (below).
   auto kb_of = [&](uint32_t w) {
     return (int)(EXACT ? (w & 0xFFFFu) : (w & 0x3FFFFFFFu));
   };
@@ -576,8 +583,14 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
     beg = sched_ptr[pq];
     n = sched_ptr[pq + 1] - beg;
   }
+  // Step j takes the row's word n-1-j: key blocks in descending order.  With
+  // the pairs of a head dispatched last to first, a workgroup started later
+  // holds keys further left, so it reaches the blocks it shares with the
+  // workgroups started before it after fewer steps of its own, while they are
+  // still in L2 (the same holds for ascending walks of ascending pairs); the
+  // key blocks every row keeps (text tokens, at the end) come first.
   auto word_at = [&](int j) -> uint32_t {   // schedule word of step j
-    return SPARSE ? sched[beg + j] : ((uint32_t)j | 0xC0000000u);
+    return SPARSE ? sched[beg + n - 1 - j] : ((uint32_t)(n - 1 - j) | 0xC0000000u);
   };
   // The word of step j+3 is fetched by a vector load one step before it is
   // needed, so the load's latency hides under a whole step (a scalar load
@@ -585,7 +598,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const __amdgpu_buffer_rsrc_t rsched =
       make_rsrc(sched, SPARSE ? (uint32_t)(sched_ptr[npairs] * 4) : 0u);
   auto word_fetch = [&](int j) -> uint32_t {   // VGPR value, clamped to the row
-    const int jj = j < n ? j : n - 1;
+    const int jj = j < n ? n - 1 - j : 0;
     if constexpr (!SPARSE) return (uint32_t)jj | 0xC0000000u;
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsched, (beg + jj) * 4, 0, 0);
   };
