@@ -172,7 +172,18 @@ void lvsa_csr_free(lvsa_csr* csr);
  *                bit  31      query block 2p+1 keeps kb
  * (the token-exact form of the words is given with lvsa_exact_mask).
  * pair_ptr[np + 1] delimits the rows (pair_ptr[0] = 0); a row holds at most
- * nb words and all rows together at most nnz. */
+ * nb words and all rows together at most nnz.
+ *
+ * On the device, pair_ptr has LVSA_PAIR_WORK more int32 words after its
+ * np + 1 offsets: the attention kernels' tile counters (workgroups take
+ * tiles dynamically, so XCDs that clock faster take on more of them).  They
+ * must be zero when a launch starts, and every launch leaves them zero: both
+ * builders zero them (lvsa_csr_upload and lvsa_build_*_device), and after
+ * that they need no care.  Attention launches that read the same device
+ * pair_ptr must not run at the same time (as two launches must not write the
+ * same output); sequential launches on one stream, and replays of a
+ * captured graph, are fine. */
+#define LVSA_PAIR_WORK 16
 
 /* Host arrays of a handle's pair schedule (valid until lvsa_csr_free):
  * np rows, n_words words, block-form words, and the token-exact words of a
@@ -192,7 +203,7 @@ typedef struct lvsa_block_mask {
   int32_t n_blocks;         /* nb = ceil(N / B)                            */
   const int32_t* row_ptr;   /* device, [nb + 1], row_ptr[0] = 0, ascending */
   const int32_t* col_idx;   /* device, [row_ptr[nb]], each row ascending   */
-  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1]                  */
+  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1 + LVSA_PAIR_WORK] */
   const uint32_t* pair_word;/* device, block-form pair words               */
 } lvsa_block_mask;
 
@@ -205,7 +216,8 @@ lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
  *   d_row_ptr     device int32[nb + 1]
  *   d_col_idx     device int32[col_capacity]; col_capacity must be at least
  *                 nb * nb (the mask's worst case), so every write is in bounds
- *   d_pair_ptr    device int32[ceil(nb / 2) + 1]
+ *   d_pair_ptr    device int32[ceil(nb / 2) + 1 + LVSA_PAIR_WORK] (offsets,
+ *                 then the work words, which this call zeroes)
  *   d_pair_word   device uint32[pair_capacity], pair_capacity at least
  *                 ceil(nb / 2) * nb; block-form words
  * Arguments as for lvsa_build_mask; T <= LVSA_MAX_FRAMES.
@@ -254,7 +266,7 @@ typedef struct lvsa_exact_mask {
   int32_t frame_tokens;     /* P >= B                                       */
   const int32_t* row_ptr;   /* device, [nb + 1], as in lvsa_block_mask      */
   const uint32_t* entry;    /* device, [row_ptr[nb]] entry words, kb ascending */
-  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1]                   */
+  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1 + LVSA_PAIR_WORK]  */
   const uint32_t* pair_word;/* device, token-exact pair words               */
 } lvsa_exact_mask;
 
@@ -283,7 +295,8 @@ lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out);
  * `stream`, into caller-owned buffers
  *   d_row_ptr    device int32[nb + 1]
  *   d_entry      device uint32[entry_capacity], entry_capacity >= nb * nb
- *   d_pair_ptr   device int32[ceil(nb / 2) + 1]
+ *   d_pair_ptr   device int32[ceil(nb / 2) + 1 + LVSA_PAIR_WORK], as for
+ *                lvsa_build_mask_device
  *   d_pair_word  device uint32[pair_capacity], pair_capacity >=
  *                ceil(nb / 2) * nb; token-exact pair words
  * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED (P < B, B > 255,
@@ -319,7 +332,9 @@ typedef struct lvsa_tensor {
  * nearest even).  q, k, v, out share heads, n_tokens = mask->n_tokens and
  * head_dim = 128; mask->block is 64 or 128.  Rows i >= N of `out` are never
  * written.  out must not overlap q, k or v.  The result is deterministic
- * (fixed key order per row).
+ * (fixed key order per row, whichever workgroup computes it).  Launches
+ * that share mask->pair_ptr must not overlap in time (its work words, see
+ * the pair schedule).
  * Errors: EINVAL (nulls, including the pair schedule, shape mismatch),
  * EUNSUPPORTED (head_dim, block, alignment), EDEVICE (launch). */
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,

@@ -23,7 +23,7 @@ __all__ = [
     "params_default", "frame_sets", "build_mask", "build_mask_device",
     "build_exact_mask_device", "attention", "attention_exact",
     "dense_attention", "WINDOW_BASIC", "WINDOW_ADAPTIVE", "WINDOW_EXPANDED",
-    "MAX_FRAMES",
+    "MAX_FRAMES", "PAIR_WORK",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -31,6 +31,7 @@ LIB_PATH = os.path.join(_HERE, "liblvsa.so")
 
 WINDOW_BASIC, WINDOW_ADAPTIVE, WINDOW_EXPANDED = 0, 1, 2
 MAX_FRAMES = 4096
+PAIR_WORK = 16   # LVSA_PAIR_WORK: work words after a device pair_ptr's offsets
 OK, EINVAL, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
 
 _i32 = ctypes.c_int32
@@ -280,8 +281,9 @@ def build_mask(T, P, B, step, params=None, layer=0, exact=False):
 
 
 def pair_buffers(n_tokens, block, device=None, stream=None):
-    """Device int32 tensors (pair_ptr [ceil(nb/2)+1], pair words
-    [ceil(nb/2)*nb]) sized for a device builder's pair schedule, allocated on
+    """Device int32 tensors (pair_ptr [ceil(nb/2)+1+PAIR_WORK]: the offsets and
+    the attention kernels' work words; pair words [ceil(nb/2)*nb]) sized for a
+    device builder's pair schedule, allocated on
     `stream` (a torch stream, a raw stream handle or None for the current
     one) so the caching allocator reuses them only after that stream's work."""
     import torch
@@ -295,8 +297,15 @@ def pair_buffers(n_tokens, block, device=None, stream=None):
     else:
         s = stream
     with torch.cuda.stream(s):
-        return (torch.empty(npairs + 1, dtype=torch.int32, device=dev),
+        return (torch.empty(npairs + 1 + PAIR_WORK, dtype=torch.int32, device=dev),
                 torch.empty(max(npairs * nb, 1), dtype=torch.int32, device=dev))
+
+
+def _check_pair_ptr(pair_ptr, N, B):
+    npairs = ((N + B - 1) // B + 1) // 2
+    if pair_ptr.numel() < npairs + 1 + PAIR_WORK:
+        raise LvsaError(EINVAL, f"pair_ptr holds {pair_ptr.numel()} words, the pair schedule "
+                        f"needs ceil(nb/2) + 1 + PAIR_WORK = {npairs + 1 + PAIR_WORK}")
 
 
 def _mask_with_pairs(mask, tensors):
@@ -313,6 +322,7 @@ def build_mask_device(T, P, B, step, row_ptr, col_idx, params=None, layer=0,
     N = T * P + params.text_tokens
     if pair_ptr is None or pair_word is None:
         pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
+    _check_pair_ptr(pair_ptr, N, B)
     _check(lib().lvsa_build_mask_device(T, P, B, step, layer, ctypes.byref(params),
                                         _p(row_ptr.data_ptr()), _p(col_idx.data_ptr()),
                                         col_idx.numel(), _p(pair_ptr.data_ptr()),
@@ -334,6 +344,7 @@ def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
     N = T * P + params.text_tokens
     if pair_ptr is None or pair_word is None:
         pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
+    _check_pair_ptr(pair_ptr, N, B)
     _check(lib().lvsa_build_exact_mask_device(
         T, P, B, step, layer, ctypes.byref(params), _p(row_ptr.data_ptr()),
         _p(entry.data_ptr()), entry.numel(), _p(pair_ptr.data_ptr()),

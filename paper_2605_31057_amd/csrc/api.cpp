@@ -81,10 +81,15 @@ namespace {
 
 // Device copy of a host array: allocated on the first upload (the handle's
 // arrays never change size), then copied asynchronously on `s`.
+// Device copy of `host` followed by `zeros` zero elements (allocated on the
+// first upload, reused after).
 template <typename T>
-lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s) {
+lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s,
+                         size_t zeros = 0) {
+  static const T kZeros[LVSA_PAIR_WORK] = {};
+  if (zeros > LVSA_PAIR_WORK) return LVSA_EINVAL;
   if (!*dev) {
-    const size_t n = host.empty() ? 1 : host.size();
+    const size_t n = (host.empty() ? 1 : host.size()) + zeros;
     if (hipMalloc(dev, sizeof(T) * n) != hipSuccess) {
       *dev = nullptr;
       return LVSA_ENOMEM;
@@ -93,6 +98,9 @@ lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s) {
   if (!host.empty() &&
       hipMemcpyAsync(*dev, host.data(), sizeof(T) * host.size(), hipMemcpyHostToDevice,
                      s) != hipSuccess)
+    return LVSA_EDEVICE;
+  if (zeros && hipMemcpyAsync(*dev + host.size(), kZeros, sizeof(T) * zeros,
+                              hipMemcpyHostToDevice, s) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -220,7 +228,8 @@ lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
   lvsa_status st;
   if ((st = upload_array(csr->row_ptr, &csr->d_row_ptr, s)) != LVSA_OK) return st;
   if ((st = upload_array(csr->col_idx, &csr->d_col_idx, s)) != LVSA_OK) return st;
-  if ((st = upload_array(csr->pair_ptr, &csr->d_pair_ptr, s)) != LVSA_OK) return st;
+  if ((st = upload_array(csr->pair_ptr, &csr->d_pair_ptr, s, LVSA_PAIR_WORK)) != LVSA_OK)
+    return st;
   if ((st = upload_array(csr->pair_word, &csr->d_pair_word, s)) != LVSA_OK) return st;
   if (csr->has_entry) {
     if ((st = upload_array(csr->entry, &csr->d_entry, s)) != LVSA_OK) return st;

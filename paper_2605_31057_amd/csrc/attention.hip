@@ -55,6 +55,8 @@
 // when a new row max exceeds it by more than 8 (p then stays below 2^8), which
 // skips most rescales of O; the result is exact either way because O and l
 // always use the same m.
+#include <atomic>
+
 #include "internal.h"
 
 namespace lvsa {
@@ -486,9 +488,11 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
 // ATTN_EXACT (token-exact schedule words).  `sched_ptr` / `sched` are the
 // pair schedule (lvsa.h): row p lists the key blocks of query blocks 2p and
 // 2p+1.
+// One tile: head `tile / npairs`, pair of query blocks from `tile % npairs`,
+// using the workgroup's LDS stages `lds` (K slots 0-1, V slots 0-1).
 template <int BLOCK, int MODE>
-__global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
-    const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
+__device__ __forceinline__ void attn_tile(
+    char* lds, int tile, const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
     const __bf16* __restrict__ vg, __bf16* __restrict__ og, int64_t q_sh,
     int64_t q_st, int64_t k_sh, int64_t k_st, int64_t v_sh, int64_t v_st,
     int64_t o_sh, int64_t o_st, int32_t H, int32_t N, int32_t nb,
@@ -497,8 +501,6 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   using TL = Tile<BLOCK>;
   constexpr bool SPARSE = MODE != ATTN_DENSE;
   constexpr bool EXACT = MODE == ATTN_EXACT;
-  // Stages: K slots 0-1, V slots 0-1.
-  __shared__ __attribute__((aligned(1024))) char lds[4 * TL::BYTES];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_void*)lds;
 
   const int tid = threadIdx.x;
@@ -508,7 +510,6 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   const int li = lane % 32;
 
   const int npairs = (nb + 1) / 2;
-  const int tile = xcd_remap(blockIdx.x, npairs * H);
   const int head = tile / npairs;
   // Pairs of a head go last to first: rows that attend every key block (text
   // tokens, placed after the video tokens) are the longest tiles, and taking
@@ -580,8 +581,10 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
 
   int beg = 0, n = nb;
   if constexpr (SPARSE) {
-    beg = sched_ptr[pq];
-    n = sched_ptr[pq + 1] - beg;
+    // Uniform by construction; the pair offsets share their array with the
+    // kernel's tile counters, so the compiler loads them per lane.
+    beg = __builtin_amdgcn_readfirstlane(sched_ptr[pq]);
+    n = __builtin_amdgcn_readfirstlane(sched_ptr[pq + 1]) - beg;
   }
   // Step j takes the row's word n-1-j: key blocks in descending order.  With
   // the pairs of a head dispatched last to first, a workgroup started later
@@ -595,8 +598,8 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   // The word of step j+3 is fetched by a vector load one step before it is
   // needed, so the load's latency hides under a whole step (a scalar load
   // would be waited for at the next LDS wait, which shares its counter).
-  const __amdgpu_buffer_rsrc_t rsched =
-      make_rsrc(sched, SPARSE ? (uint32_t)(sched_ptr[npairs] * 4) : 0u);
+  const __amdgpu_buffer_rsrc_t rsched = make_rsrc(
+      sched, SPARSE ? (uint32_t)__builtin_amdgcn_readfirstlane(sched_ptr[npairs] * 4) : 0u);
   auto word_fetch = [&](int j) -> uint32_t {   // VGPR value, clamped to the row
     const int jj = j < n ? n - 1 - j : 0;
     if constexpr (!SPARSE) return (uint32_t)jj | 0xC0000000u;
@@ -709,16 +712,132 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(
   }
 }
 
+// First tile and tile count of XCD x's share of `total` tiles (contiguous,
+// as xcd_remap deals them).
+__device__ __forceinline__ int xcd_first(int x, int total) {
+  const int per = total / 8, rem = total % 8;
+  return x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
+}
+__device__ __forceinline__ int xcd_count(int x, int total) {
+  return total / 8 + (x < total % 8 ? 1 : 0);
+}
+
+// Next tile for a workgroup on XCD `xcd`: the next one of its own XCD's share
+// (ctr[x] counts the tiles handed out of XCD x's share), else the next one of
+// another XCD's share, so XCDs that run faster take on more tiles; -1 when
+// every share is handed out.  Every call advances at most 8 counters by one,
+// so a workgroup's loop ends after at most total + 8 calls.
+__device__ __forceinline__ int fetch_tile(uint32_t* ctr, int xcd, int total) {
+  for (int d = 0; d < 8; ++d) {
+    const int x = (xcd + d) % 8;
+    const uint32_t cnt = (uint32_t)xcd_count(x, total);
+    if (__hip_atomic_load(&ctr[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= cnt)
+      continue;
+    const uint32_t c = atomicAdd(&ctr[x], 1u);
+    if (c < cnt) return xcd_first(x, total) + (int)c;
+  }
+  return -1;
+}
+
+// Kernel arguments, passed as one struct so that the persistent loop can
+// read them again for every tile instead of holding them in registers.
+struct KArgs {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  __bf16* o;
+  int64_t q_sh, q_st, k_sh, k_st, v_sh, v_st, o_sh, o_st;
+  const int32_t* sched_ptr;
+  const uint32_t* sched;
+  int32_t H, N, nb, P;
+  float scale_log2;
+};
+
+template <int BLOCK, int MODE>
+__device__ __forceinline__ void attn_tile_args(char* lds, int tile, const KArgs& a) {
+  attn_tile<BLOCK, MODE>(lds, tile, a.q, a.k, a.v, a.o, a.q_sh, a.q_st, a.k_sh, a.k_st,
+                         a.v_sh, a.v_st, a.o_sh, a.o_st, a.H, a.N, a.nb, a.sched_ptr,
+                         a.sched, a.P, a.scale_log2);
+}
+
+// Block-sparse and token-exact attention: persistent workgroups, one per CU,
+// take tiles until all are done; ctr (16 words after the pair schedule's
+// offsets, zero on entry) holds the 8 per-XCD tile counters and the count of
+// finished workgroups, and the last workgroup to finish sets them back to
+// zero.  Dense attention: one workgroup per tile, dealt to XCDs by
+// xcd_remap.  `sched_ptr` / `sched` are the pair schedule (lvsa.h).
+template <int BLOCK, int MODE>
+__global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(const KArgs args) {
+  __shared__ __attribute__((aligned(1024))) char lds[4 * Tile<BLOCK>::BYTES];
+  const int npairs = (args.nb + 1) / 2;
+  const int total = npairs * args.H;
+  if constexpr (MODE == ATTN_DENSE) {
+    attn_tile_args<BLOCK, MODE>(lds, xcd_remap(blockIdx.x, total), args);
+  } else {
+    __shared__ int next_tile;
+    uint32_t* const ctr = (uint32_t*)(const_cast<int32_t*>(args.sched_ptr) + npairs + 1);
+    // Workgroups are dispatched round-robin over the 8 XCDs.
+    const int xcd = blockIdx.x % 8;
+    for (;;) {
+      if (threadIdx.x == 0) next_tile = fetch_tile(ctr, xcd, total);
+      __syncthreads();
+      const int tile = __builtin_amdgcn_readfirstlane(next_tile);
+      __syncthreads();   // every wave has read next_tile before it is rewritten
+      if (tile < 0) break;
+      // The arguments are the first kernel argument; an offset the compiler
+      // cannot see to be zero makes every tile load them afresh (scalar
+      // loads), so they are not live across tiles.
+      int zero = 0;
+      asm volatile("" : "+v"(zero));
+      zero = __builtin_amdgcn_readfirstlane(zero);
+      const KArgs* ap = (const KArgs*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() + zero);
+      attn_tile_args<BLOCK, MODE>(lds, tile, *ap);
+    }
+    if (threadIdx.x == 0) {
+      __threadfence();
+      if (atomicAdd(&ctr[8], 1u) == gridDim.x - 1) {
+        __threadfence();
+        for (int x = 0; x < 9; ++x) atomicExch(&ctr[x], 0u);
+      }
+    }
+  }
+}
+
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
 template <int BLOCK, int MODE>
 hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)D);
-  const int grid = (a.n_blocks + 1) / 2 * a.heads;
-  hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, MODE>), dim3(grid),
-                     dim3(Tile<BLOCK>::NT), 0, stream, (const __bf16*)a.q,
-                     (const __bf16*)a.k, (const __bf16*)a.v, (__bf16*)a.o,
-                     a.q_sh, a.q_st, a.k_sh, a.k_st, a.v_sh, a.v_st, a.o_sh,
-                     a.o_st, a.heads, a.n_tokens, a.n_blocks, a.pair_ptr,
-                     a.pair_word, a.frame_tokens, scale_log2);
+  const int tiles = (a.n_blocks + 1) / 2 * a.heads;
+  // Block-sparse and token-exact: one persistent workgroup per CU (each
+  // takes 128 KB of LDS, so one fits a CU); dense: one workgroup per tile.
+  const int grid = MODE == ATTN_DENSE ? tiles : (tiles < cu_count() ? tiles : cu_count());
+  KArgs k;
+  k.q = (const __bf16*)a.q;
+  k.k = (const __bf16*)a.k;
+  k.v = (const __bf16*)a.v;
+  k.o = (__bf16*)a.o;
+  k.q_sh = a.q_sh; k.q_st = a.q_st; k.k_sh = a.k_sh; k.k_st = a.k_st;
+  k.v_sh = a.v_sh; k.v_st = a.v_st; k.o_sh = a.o_sh; k.o_st = a.o_st;
+  k.sched_ptr = a.pair_ptr;
+  k.sched = a.pair_word;
+  k.H = a.heads; k.N = a.n_tokens; k.nb = a.n_blocks; k.P = a.frame_tokens;
+  k.scale_log2 = scale_log2;
+  hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, MODE>), dim3(grid), dim3(Tile<BLOCK>::NT), 0,
+                     stream, k);
   return hipGetLastError();
 }
 

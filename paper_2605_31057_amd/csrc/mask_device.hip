@@ -142,6 +142,8 @@ __global__ __launch_bounds__(kRowThreads) void count_rows_kernel(
     if (p == 0) {
       row_ptr[0] = 0;
       pair_ptr[0] = 0;
+      // The attention kernel's work words after the offsets start at zero.
+      for (int i = 0; i < LVSA_PAIR_WORK; ++i) pair_ptr[gridDim.x + 1 + i] = 0;
     }
   }
 }

@@ -424,3 +424,21 @@ def test_host_builder_text_on_hv_horizon():
     out = ctypes.c_void_p()
     assert L.lib().lvsa_build_mask(65, 1590, 128, 0, 0, ctypes.byref(bad),
                                    ctypes.byref(out)) == L.EINVAL
+
+
+def test_device_builder_binding_rejects_short_pair_ptr():
+    """The device pair_ptr carries PAIR_WORK work words after its offsets; the
+    binding refuses a buffer without them before any library call."""
+    import torch
+    T, P, B = 4, 256, 64
+    nb = -(-T * P // B)
+    npairs = (nb + 1) // 2
+    rp = torch.empty(nb + 1, dtype=torch.int32)
+    ci = torch.empty(nb * nb, dtype=torch.int32)
+    pw = torch.empty(npairs * nb, dtype=torch.int32)
+    p = L.Params(budget_frames=2, window=0, tper=4)
+    for build, second in ((L.build_mask_device, ci), (L.build_exact_mask_device, ci)):
+        with pytest.raises(L.LvsaError) as e:
+            build(T, P, B, 0, rp, second, params=p,
+                  pair_ptr=torch.empty(npairs + 1, dtype=torch.int32), pair_word=pw)
+        assert e.value.status == L.EINVAL

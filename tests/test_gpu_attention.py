@@ -269,3 +269,41 @@ def test_pairs_whose_rows_differ(T, P, B, exact):
     torch.cuda.synchronize()
     err = np.abs(out.float().cpu().numpy() - ref)
     assert_close(float(err.max()), float(err.mean()))
+
+
+@pytest.mark.parametrize("T,P,B,H", [
+    (20, 512, 128, 8),    # 40 pairs x 8 heads = 320 tiles: more tiles than CUs
+    (6, 200, 64, 1),      # 10 tiles: fewer tiles than CUs
+])
+def test_tile_counters_left_zero_and_results_repeat(T, P, B, H):
+    """Workgroups take tiles through counters kept after the pair offsets;
+    every launch must leave them zero, so back-to-back launches on one mask
+    (block and token-exact forms) give identical outputs, matching the
+    oracle."""
+    N = T * P
+    nb = -(-N // B)
+    npairs = (nb + 1) // 2
+    _say(f"[counters] T={T} P={P} B={B} H={H}: {npairs * H} tiles")
+    q, k, v = make_qkv(H, N, seed=T * 7 + P)
+    qd, kd, vd = (x.cuda() for x in (q, k, v))
+    p = L.Params(budget_frames=7, window=1)
+    rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+    ci = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+    pp, pw = L.pair_buffers(N, B)
+    ppx, pwx = L.pair_buffers(N, B)
+    m = L.build_mask_device(T, P, B, 2, rp, ci, params=p, pair_ptr=pp, pair_word=pw)
+    me = L.build_exact_mask_device(T, P, B, 2, rp.clone(), ent, params=p, pair_ptr=ppx,
+                                   pair_word=pwx)
+    outs, outs_x = [], []
+    for _ in range(3):
+        outs.append(L.attention(qd, kd, vd, m))
+        outs_x.append(L.attention_exact(qd, kd, vd, me))
+    torch.cuda.synchronize()
+    assert bool((pp[npairs + 1:] == 0).all()) and bool((ppx[npairs + 1:] == 0).all())
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
+    for o in outs_x[1:]:
+        assert torch.equal(o, outs_x[0])
+    rpo, cio = M.build_mask(T, P, B, 2, C=7, W=1)
+    assert_close(*compare_rows(outs[0], q, k, v, rpo, cio, B, range(H), range(nb)))

@@ -131,7 +131,8 @@ def test_device_exact_builder_matches_host(name):
     p = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper)
     rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
     ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
-    pp = torch.empty((nb + 1) // 2 + 1, dtype=torch.int32, device="cuda")
+    npairs = (nb + 1) // 2
+    pp = torch.full((npairs + 1 + L.PAIR_WORK,), -1, dtype=torch.int32, device="cuda")
     pw = torch.empty((nb + 1) // 2 * nb, dtype=torch.int32, device="cuda")
     for step in (0, 3, 10):
         _say(f"[exact-builder] {name} step {step}")
@@ -145,7 +146,8 @@ def test_device_exact_builder_matches_host(name):
         assert np.array_equal(got, he)
         # token-exact pair schedule, bit for bit against the host's
         hpp, _, hpe = csr.pairs()
-        assert np.array_equal(pp.cpu().numpy(), hpp)
+        assert np.array_equal(pp[:npairs + 1].cpu().numpy(), hpp)
+        assert bool((pp[npairs + 1:] == 0).all())   # work words zeroed
         assert np.array_equal(pw[:int(hpp[-1])].cpu().numpy().view(np.uint32), hpe)
 
 

@@ -29,7 +29,8 @@ def _device_csr(T, P, B, step, p, layer=0):
     nb = -(-(T * P + p.text_tokens) // B)
     rp = torch.full((nb + 1,), -1, dtype=torch.int32, device="cuda")
     ci = torch.full((nb * nb,), -1, dtype=torch.int32, device="cuda")
-    pp = torch.full(((nb + 1) // 2 + 1,), -1, dtype=torch.int32, device="cuda")
+    npairs = (nb + 1) // 2
+    pp = torch.full((npairs + 1 + L.PAIR_WORK,), -1, dtype=torch.int32, device="cuda")
     pw = torch.full(((nb + 1) // 2 * nb,), -1, dtype=torch.int32, device="cuda")
     L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer, pair_ptr=pp,
                         pair_word=pw)
@@ -37,6 +38,9 @@ def _device_csr(T, P, B, step, p, layer=0):
     rp = rp.cpu()
     nnz = int(rp[-1])
     pp = pp.cpu()
+    # the attention kernels' work words after the offsets are zeroed
+    assert bool((pp[npairs + 1:] == 0).all())
+    pp = pp[:npairs + 1]
     words = pw[:int(pp[-1])].cpu().numpy().view(np.uint32)
     # nothing written past the pair words either
     assert bool((pw[int(pp[-1]):] == -1).all())
