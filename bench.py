@@ -327,10 +327,24 @@ def main():
         print("[bench] dense", file=sys.stderr, flush=True)
         d_ms = median(time_calls(lambda: L.dense_attention(q, k, v, block=w.block,
                                                            out=out, stream=stream), 5, 1))
+        # Dense attention also through the block-sparse kernel with a full
+        # mask (a window of T frames keeps every block), which takes tiles
+        # dynamically across XCDs as the sparse launch does; the speedup is
+        # taken against the faster of the two dense timings.
+        full = L.Params(budget_frames=w.budget_frames, window=w.frames, tper=w.frames,
+                        text_tokens=w.text_tokens)
+        mf = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
+                                 params=full, stream=stream)
+        torch.cuda.synchronize()
+        assert int(rp[-1]) == nb * nb, "full mask expected"
+        f_ms = median(time_calls(lambda: L.attention(q, k, v, mf, out=out, stream=stream),
+                                 5, 1))
+        base = min(d_ms, f_ms)
         dense = {
             "dense_ms_per_call": d_ms,
-            "dense_tflops": dense_flops / (d_ms * 1e-3) / 1e12,
-            "speedup_vs_dense": d_ms / attn_med,
+            "dense_full_mask_ms_per_call": f_ms,
+            "dense_tflops": dense_flops / (base * 1e-3) / 1e12,
+            "speedup_vs_dense": base / attn_med,
             "inv_density": dense_flops / flops_of[s_ref],
         }
 
