@@ -122,7 +122,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 10400; }
+int32_t lvsa_version(void) { return 10500; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
