@@ -333,16 +333,20 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid
 // width: per score one add of a constant, one compare into VCC and one
 // select.  A scheduling barrier every 4 scores keeps the compiler from
 // computing many compare results ahead (each holds an SGPR pair).
+//
+// The lane's query row lies in the second frame iff its row index within the
+// wave's 32 rows reaches `sec_from` (wave-uniform); the lane index is
+// recomputed here rather than held in a register through the loop.
 template <int BLOCK>
-__device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, int lane, uint32_t pat,
-                                           int kfirst, int valid,
-                                           const bool (&second)[QT]) {
+__device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, uint32_t pat, int kfirst,
+                                           int valid, const int (&sec_from)[QT]) {
   using TL = Tile<BLOCK>;
-  const int hl = lane / 32;
   if (pat != 0xFu || valid < BLOCK) {
+    const int lane = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    const int hl = lane / 32, li = lane % 32;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      const uint32_t bits = second[qt] ? pat >> 2 : pat;
+      const uint32_t bits = li >= sec_from[qt] ? pat >> 2 : pat;
       const int klo = (bits & 1u) ? 0 : kfirst;
       const int khi = (bits & 2u) ? valid : min(kfirst, valid);
       const uint32_t shift = (uint32_t)(4 * hl - klo);
@@ -555,16 +559,17 @@ __device__ __forceinline__ void attn_tile(
                         : bf16x8{};
   }
 
-  // Exact mode: whether each of the lane's query rows lies in the query
-  // block's second frame (the first frame holds the block's first qfirst
-  // rows; P >= BLOCK, so there are at most two).
-  bool second[QT];
+  // Exact mode: the first of the wave's 32 rows (per q tile) that lies in
+  // the query block's second frame (the first frame holds the block's first
+  // qfirst rows; P >= BLOCK, so there are at most two); wave-uniform.
+  int sec_from[QT];
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) second[qt] = false;
+  for (int qt = 0; qt < QT; ++qt) sec_from[qt] = 32;
   if constexpr (EXACT) {
     const int qfirst = P - (int)(((int64_t)qb * BLOCK) % P);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) second[qt] = rows0 + 32 * qt + li >= qfirst;
+    for (int qt = 0; qt < QT; ++qt)
+      sec_from[qt] = __builtin_amdgcn_readfirstlane(qfirst - rows0 - 32 * qt);
   }
   // Masks the scores of the key block of schedule word w for this wave's
   // query block: a key block that block does not keep has no valid keys.
@@ -573,8 +578,8 @@ __device__ __forceinline__ void attn_tile(
   auto mask_block = [&](Scores<BLOCK>& sc, uint32_t w) {
     const int kb = kb_of(w);
     if constexpr (EXACT)
-      mask_exact<BLOCK>(sc, lane, (w >> pat_shift) & 0xFu, (int)((w >> 16) & 0xFFu),
-                        N - kb * BLOCK, second);
+      mask_exact<BLOCK>(sc, (w >> pat_shift) & 0xFu, (int)((w >> 16) & 0xFFu),
+                        N - kb * BLOCK, sec_from);
     else
       mask_tail<BLOCK>(sc, lane, ((w >> kept_bit) & 1u) ? N - kb * BLOCK : 0);
   };
