@@ -211,7 +211,7 @@ typedef struct lvsa_block_mask {
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
 
 /* Device builder: the same mask and its pair schedule computed on the GPU
- * (six short kernels on `stream`), written to caller-owned device buffers
+ * (four short kernels on `stream`), written to caller-owned device buffers
  * (no host round trip, no allocation).
  *   d_row_ptr     device int32[nb + 1]
  *   d_col_idx     device int32[col_capacity]; col_capacity must be at least
