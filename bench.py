@@ -32,7 +32,8 @@ PEAK_HBM_GBS = 8000.0
 METRIC = ("ms/attention call + effective TFLOP/s (kept blocks) and speedup vs "
           "dense, Wan-1.3B 6×")
 ATTN_SRC = os.path.join(ROOT, "paper_2605_31057_amd", "csrc", "attention.hip")
-PMC_FILE = os.path.join(ROOT, "profiles", "attn_sparse_wan13_6x_pmc.json")
+PROFILES = os.path.join(ROOT, "profiles")
+SPARSE_KERNEL = "attn_fwd_kernel<128, ATTN_BLOCK>"
 
 
 def kept_flops(row_ptr, col_idx, n_tokens, block, heads, d=128):
@@ -76,17 +77,72 @@ def time_calls(fn, n, warm):
     return [a.elapsed_time(b) for a, b in evs]
 
 
-def traffic_from_profile():
-    """HBM bytes per sparse launch from the committed PMC summary, if it was
-    taken on the current kernel source (else None)."""
-    if not os.path.exists(PMC_FILE):
+def percentile(xs, q):
+    xs = sorted(xs)
+    return xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]
+
+
+def traffic_from_profile(workload, kernel):
+    """HBM bytes per launch of `kernel` at `workload` from the committed PMC
+    summary of that workload (profiles/pmc_<workload>.json), if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"pmc_{workload}.json")
+    if not os.path.exists(path):
         return None
-    with open(PMC_FILE) as f:
+    with open(path) as f:
         rec = json.load(f)
     src = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
-    if rec.get("attention_src_sha256") != src:
+    if rec.get("attention_src_sha256") != src or rec.get("workload") != workload:
         return None
-    return rec.get("hbm_bytes_per_launch")
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def host_cores():
+    """Logical CPUs this process may run on, and physical cores among them
+    (from /proc/cpuinfo; None where it cannot be read)."""
+    logical = len(os.sched_getaffinity(0))
+    try:
+        cores = set()
+        phys = core = None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("physical id"):
+                    phys = line.split(":")[1].strip()
+                elif line.startswith("core id"):
+                    core = line.split(":")[1].strip()
+                elif not line.strip() and core is not None:
+                    cores.add((phys, core))
+                    phys = core = None
+        physical = len(cores) or None
+    except OSError:
+        physical = None
+    return logical, physical
+
+
+def metadata_costs(w, L, params, reps=200):
+    """Sec. 2 metadata figures: Alg. 1 growth steps (max, mean over every
+    query frame of every swept step), the per-frame window call and the host
+    CSR rebuild."""
+    grow = []
+    for s in w.steps:
+        grow += L.frame_sets(w.frames, s, params, growth=True)[4]
+    T = w.frames
+    t0 = time.perf_counter()
+    for i in range(reps):
+        L.frame_sets(w.frames, w.steps[i % len(w.steps)], params)
+    per_frame_us = (time.perf_counter() - t0) / (reps * T) * 1e6
+    t0 = time.perf_counter()
+    for i in range(reps):
+        L.frame_window(w.frames, w.steps[i % len(w.steps)], i % T, params)
+    per_call_us = (time.perf_counter() - t0) / reps * 1e6
+    return {
+        "alg1_growth_max": max(grow),
+        "alg1_growth_mean": sum(grow) / len(grow),
+        "alg1_frames_counted": len(grow),
+        "frame_window_us_per_frame": per_frame_us,
+        "frame_window_us_per_call_via_python": per_call_us,
+    }
 
 
 def cpu_baseline(w, target_s):
@@ -98,9 +154,10 @@ def cpu_baseline(w, target_s):
     from oracle import mask as M
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        cores = os.cpu_count()
+        threads = os.cpu_count()
+    logical, physical = host_cores()
     t0 = time.perf_counter()
     rp, ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, 10,
                           C=w.budget_frames, W=w.window, tper=w.tper,
@@ -124,14 +181,20 @@ def cpu_baseline(w, target_s):
         rows = min(w.block, n - qb * w.block)
         cols = sum(min(w.block, n - kb * w.block) for kb in ci[rp[qb]:rp[qb + 1]])
         flops += 4.0 * 128 * rows * cols
+    total = kept_flops(rp, ci, w.n_tokens, w.block, w.heads)
     return {
         "value": flops / elapsed / 1e12,
         "unit": "TFLOP/s",
-        "cores": cores,
+        "cores": threads,
         "kind": "oracle",
-        "sample": (f"{len(done)} query blocks of head 0 (step 10, fp32 numpy "
-                   f"masked softmax), {elapsed:.1f} s; oracle mask build "
-                   f"{mask_s * 1e3:.0f} ms"),
+        "sample": (f"{len(done)} of {len(rp) - 1} query blocks of head 0 of {w.heads} "
+                   f"(step 10, fp32 numpy masked softmax), {elapsed:.1f} s; a rate "
+                   f"measured on that sample: the whole call ({total:.3g} FLOP) would take "
+                   f"{total / (flops / elapsed):.0f} s at it (extrapolated, not run); "
+                   f"oracle mask build {mask_s * 1e3:.0f} ms"),
+        "threads": threads,
+        "logical_cpus": logical,
+        "physical_cores": physical,
     }
 
 
@@ -234,6 +297,8 @@ def main():
     attn_ms = time_calls(lambda: L.attention(q, k, v, m, out=out, stream=stream),
                          20, 3)
     attn_med = median(attn_ms)
+    spread = {"p10": percentile(attn_ms, 0.1), "p90": percentile(attn_ms, 0.9),
+              "min": min(attn_ms), "max": max(attn_ms), "calls": len(attn_ms)}
     # Cold caches: before each timed call, overwrite a 1 GiB buffer (more than
     # the L2s and the 256 MB last-level cache hold) so Q, K, V start in HBM.
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
@@ -328,9 +393,8 @@ def main():
         d_ms = median(time_calls(lambda: L.dense_attention(q, k, v, block=w.block,
                                                            out=out, stream=stream), 5, 1))
         # Dense attention also through the block-sparse kernel with a full
-        # mask (a window of T frames keeps every block), which takes tiles
-        # dynamically across XCDs as the sparse launch does; the speedup is
-        # taken against the faster of the two dense timings.
+        # mask (a window of T frames keeps every block), reported beside the
+        # dense entry point; the speedup divides by the dense entry point.
         full = L.Params(budget_frames=w.budget_frames, window=w.frames, tper=w.frames,
                         text_tokens=w.text_tokens)
         mf = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
@@ -339,17 +403,17 @@ def main():
         assert int(rp[-1]) == nb * nb, "full mask expected"
         f_ms = median(time_calls(lambda: L.attention(q, k, v, mf, out=out, stream=stream),
                                  5, 1))
-        base = min(d_ms, f_ms)
         dense = {
             "dense_ms_per_call": d_ms,
             "dense_full_mask_ms_per_call": f_ms,
-            "dense_tflops": dense_flops / (base * 1e-3) / 1e12,
-            "speedup_vs_dense": base / attn_med,
+            "dense_tflops": dense_flops / (d_ms * 1e-3) / 1e12,
+            "speedup_vs_dense": d_ms / attn_med,
             "inv_density": dense_flops / flops_of[s_ref],
         }
 
     achieved = flops_of[s_ref] / (attn_med * 1e-3) / 1e12
-    traffic = traffic_from_profile()
+    traffic = traffic_from_profile(w.name, SPARSE_KERNEL)
+    meta = metadata_costs(w, L, params)
     rec = {
         "metric": METRIC,
         "value": value,
@@ -375,17 +439,20 @@ def main():
             "parallelism": "single GPU",
         },
         "ms_per_attention_call": attn_med,
+        "ms_per_attention_call_spread": spread,
         "ms_per_attention_call_cold_caches": median(cold),
         "attention_tflops_kept": achieved,
         "mask_build_device_us": median(mask_ms) * 1e3,
         "mask_build_host_us": median(host_us),
+        "mask_build_host_us_p90": percentile(host_us, 0.9),
+        **meta,
         "nnz_step10": nnz_of[s_ref],
         "block_density_step10": nnz_of[s_ref] / (nb * nb),
         **exact,
         **({"pattern_variants": variants} if variants else {}),
         **dense,
         "roofline": {
-            "kernel": "attn_fwd_kernel<128, ATTN_BLOCK>",
+            "kernel": SPARSE_KERNEL,
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

@@ -13,11 +13,11 @@
  * The library has two halves:
  *   - mask builders that turn (T, P, block, step, params) into per-query-block
  *     lists of kept key blocks (a block CSR), on the host (lvsa_build_mask)
- *     or on the device (lvsa_build_mask_device), together with the same mask
- *     arranged per pair of query blocks (the pair schedule the kernel reads);
+ *     or on the device (lvsa_build_mask_device);
  *   - a block-sparse flash-attention forward pass that visits only the kept
- *     blocks (lvsa_attention), and a dense pass of the same design over every
- *     block (lvsa_dense_attention, Eq. 1) used as the speed baseline.
+ *     blocks of any block CSR (lvsa_attention), and a dense pass of the same
+ *     design over every block (lvsa_dense_attention, Eq. 1) used as the speed
+ *     baseline.
  *
  * Conventions for every call:
  *   - Every function returns an lvsa_status (int32_t).  No C++ exception
@@ -107,17 +107,28 @@ void lvsa_params_default(lvsa_params* p);
  *           conditional and unconditional passes)
  * Outputs (host memory, caller-owned; any may be NULL to skip it):
  *   tper_out      the anchor period T_per used
- *   anchors       [T] ascending anchor frames; *n_anchors = |G^s| = ceil(T/T_per)
- *                 plus the extra anchors 0..E-1 that Eq. 3 did not place
+ *   anchors       [T] ascending anchor frames; *n_anchors = |G^s| (Eq. 3:
+ *                 ceil(T/T_per) distinct frames, or 1 when T_per > T) plus
+ *                 the extra anchors 0..E-1 that Eq. 3 did not place
  *   win_lo/win_hi [T] window bounds per query frame, so that
  *                 A(t) = anchors  U  [win_lo[t], win_hi[t]]
+ *   growth        [T] Alg. 1 growth steps per query frame (frames added to
+ *                 the adaptive window; 0 for the other window rules)
  * Errors: EINVAL for T, step or params out of range (including C <= 2W+1+E
  * with tper == 0, E < 0, and a null params pointer). */
 #define LVSA_MAX_FRAMES 4096
 lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
                             int32_t* tper_out, int32_t* anchors,
                             int32_t* n_anchors, int32_t* win_lo,
-                            int32_t* win_hi);
+                            int32_t* win_hi, int32_t* growth);
+
+/* The window of one query frame t (0 <= t < T) at step s: the per-frame call
+ * whose cost Sec. 2 quotes (the remark after Alg. 1).  Writes lo, hi and the
+ * Alg. 1 growth steps (any output may be NULL).  Errors as for
+ * lvsa_frame_sets, and EINVAL for t out of range. */
+lvsa_status lvsa_frame_window(int32_t T, int32_t step, const lvsa_params* p,
+                              int32_t t, int32_t* lo, int32_t* hi,
+                              int32_t* growth);
 
 /* ---------------------------------------------------------- block CSR ---- */
 
@@ -145,81 +156,57 @@ lvsa_status lvsa_build_mask(int32_t T, int32_t P, int32_t B, int32_t step,
                             int32_t layer, const lvsa_params* p,
                             lvsa_csr** out);
 
-/* Read-only view of a handle's host arrays (pointers stay valid until
- * lvsa_csr_free).  Any output pointer may be NULL. */
-lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
-                          int32_t* block, int32_t* n_blocks, int64_t* nnz,
+/* Read-only view of a handle's host CSR: nb query-block rows over nb key
+ * blocks (n_q_blocks = n_kv_blocks = nb for self-attention), nnz kept blocks,
+ * row_ptr[nb + 1] and col_idx[nnz] (valid until lvsa_csr_free).  Any output
+ * pointer may be NULL.  Errors: EINVAL (null handle). */
+lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_q_blocks,
+                          int32_t* n_kv_blocks, int64_t* nnz,
                           const int32_t** row_ptr, const int32_t** col_idx);
 
-/* Copies the host arrays, the pair schedule (below) and, when the handle has
- * them, the token-exact entry words and pair words to device memory owned by
- * the handle (allocated on the first call, on the current device),
- * asynchronously on `stream`; the host arrays must stay unmodified until the
- * stream reaches the copy, which lvsa_csr_free respects by synchronizing the
- * device before releasing.  Errors: EINVAL (null), ENOMEM, EDEVICE. */
+/* Tokens N and block size B of a handle.  Errors: EINVAL (null handle). */
+lvsa_status lvsa_csr_shape(const lvsa_csr* csr, int32_t* n_tokens, int32_t* block);
+
+/* Copies the host arrays (and, for a handle built by lvsa_build_exact_mask,
+ * its entry words) to device memory owned by the handle, allocated in the
+ * order of `stream` on the first call and reused after, asynchronously on
+ * `stream`; the handle keeps its host arrays until lvsa_csr_free, which waits
+ * for this copy.  Errors: EINVAL (null), ENOMEM, EDEVICE. */
 lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream);
 
-/* Releases host and device memory of the handle.  NULL is accepted. */
+/* Releases the handle.  Waits (on the host) for the handle's last upload to
+ * finish, then releases its device arrays in the order of the stream given
+ * to that upload, which must still exist; no device-wide synchronization.
+ * Attention launches on other streams that read the device arrays must have
+ * finished, as for any buffer that is freed.  NULL is accepted. */
 void lvsa_csr_free(lvsa_csr* csr);
 
-/* Pair schedule: the same mask arranged for the attention kernel, which
- * handles query blocks two at a time.  Row p (p < np = ceil(nb / 2)) lists,
- * in ascending order and without repeats, the key blocks kept by query
- * block 2p or by 2p+1 (the union of CSR rows 2p and 2p+1; the last row of an
- * odd nb has one query block), one 32-bit word each:
- *   block form   bits  0..29  kb
- *                bit  30      query block 2p keeps kb
- *                bit  31      query block 2p+1 keeps kb
- * (the token-exact form of the words is given with lvsa_exact_mask).
- * pair_ptr[np + 1] delimits the rows (pair_ptr[0] = 0); a row holds at most
- * nb words and all rows together at most nnz.
- *
- * On the device, pair_ptr has LVSA_PAIR_WORK more int32 words after its
- * np + 1 offsets: the attention kernels' tile counters (workgroups take
- * tiles dynamically, so XCDs that clock faster take on more of them).  They
- * must be zero when a launch starts, and every launch leaves them zero: both
- * builders zero them (lvsa_csr_upload and lvsa_build_*_device), and after
- * that they need no care.  Attention launches that read the same device
- * pair_ptr must not run at the same time (as two launches must not write the
- * same output); sequential launches on one stream, and replays of a
- * captured graph, are fine. */
-#define LVSA_PAIR_WORK 16
-
-/* Host arrays of a handle's pair schedule (valid until lvsa_csr_free):
- * np rows, n_words words, block-form words, and the token-exact words of a
- * handle built by lvsa_build_exact_mask (NULL otherwise).  Any output pointer
- * may be NULL.  Errors: EINVAL (null handle). */
-lvsa_status lvsa_csr_pairs(const lvsa_csr* csr, int32_t* n_pairs, int64_t* n_words,
-                           const int32_t** pair_ptr, const uint32_t** pair_word,
-                           const uint32_t** pair_exact);
-
-/* Device-resident block mask: the CSR and its pair schedule, which is what
- * the attention kernel reads.  Fill it from an uploaded handle with
- * lvsa_csr_device_view, or point it at buffers written by
- * lvsa_build_mask_device. */
+/* A block CSR in device memory: the mask lvsa_attention reads.  Any valid
+ * CSR works (the builders' masks, or a caller's own): row_ptr[0] = 0,
+ * row_ptr non-decreasing, nnz = row_ptr[n_q_blocks] < 2^30, each row's
+ * col_idx strictly ascending within [0, n_kv_blocks).  The kernels only
+ * read it, so launches on any streams may share one mask.  Column values
+ * outside [0, n_kv_blocks) are skipped; a row whose entries are not
+ * ascending gives an unspecified result, never a read outside row_ptr's
+ * range. */
 typedef struct lvsa_block_mask {
   int32_t n_tokens;         /* N                                           */
   int32_t block;            /* B, tokens per query block and per key block */
-  int32_t n_blocks;         /* nb = ceil(N / B)                            */
-  const int32_t* row_ptr;   /* device, [nb + 1], row_ptr[0] = 0, ascending */
-  const int32_t* col_idx;   /* device, [row_ptr[nb]], each row ascending   */
-  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1 + LVSA_PAIR_WORK] */
-  const uint32_t* pair_word;/* device, block-form pair words               */
+  int32_t n_q_blocks;       /* nb = ceil(N / B)                            */
+  int32_t n_kv_blocks;      /* nb (self-attention: the same blocks)        */
+  const int32_t* row_ptr;   /* device, [n_q_blocks + 1]                    */
+  const int32_t* col_idx;   /* device, [row_ptr[n_q_blocks]]               */
 } lvsa_block_mask;
 
-/* Errors: EINVAL if the handle was never uploaded. */
+/* Device view of an uploaded handle.  Errors: EINVAL if never uploaded. */
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out);
 
-/* Device builder: the same mask and its pair schedule computed on the GPU
- * (four short kernels on `stream`), written to caller-owned device buffers
- * (no host round trip, no allocation).
+/* Device builder: the same CSR computed on the GPU (three short kernels on
+ * `stream`), written to caller-owned device buffers (no host round trip, no
+ * allocation, no memset).
  *   d_row_ptr     device int32[nb + 1]
  *   d_col_idx     device int32[col_capacity]; col_capacity must be at least
  *                 nb * nb (the mask's worst case), so every write is in bounds
- *   d_pair_ptr    device int32[ceil(nb / 2) + 1 + LVSA_PAIR_WORK] (offsets,
- *                 then the work words, which this call zeroes)
- *   d_pair_word   device uint32[pair_capacity], pair_capacity at least
- *                 ceil(nb / 2) * nb; block-form words
  * Arguments as for lvsa_build_mask; T <= LVSA_MAX_FRAMES.
  * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED when a query-block
  * pair would touch more than 1024 frames (2B/P + 2 > 1024 and T > 1024),
@@ -228,8 +215,7 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
                                    int32_t step, int32_t layer,
                                    const lvsa_params* p, int32_t* d_row_ptr,
                                    int32_t* d_col_idx, int64_t col_capacity,
-                                   int32_t* d_pair_ptr, uint32_t* d_pair_word,
-                                   int64_t pair_capacity, void* stream);
+                                   void* stream);
 
 /* ------------------------------------------------ token-exact form ---- */
 
@@ -251,23 +237,15 @@ lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
  *                A(a ? f1 : f0)
  *   bits 28..31  zero
  * Query token i of qb attends key token j of kb iff pattern bit
- * 2*(segment(i) != f0) + (segment(j) != g0) is set.
- *
- * Token-exact pair words (the pair schedule's rows, as in the block form):
- *   bits  0..15  kb
- *   bits 16..23  kfirst
- *   bits 24..27  pattern of (2p, kb), 0 when 2p does not keep kb
- *   bits 28..31  pattern of (2p+1, kb), 0 when 2p+1 does not keep kb
- * (a kept block's pattern is never 0). */
+ * 2*(segment(i) != f0) + (segment(j) != g0) is set; segment(i) != f0 holds
+ * iff i mod P < (qb*B) mod P, i.e. query rows split at multiples of P. */
 typedef struct lvsa_exact_mask {
-  int32_t n_tokens;         /* N = T*P                                      */
+  int32_t n_tokens;         /* N                                            */
   int32_t block;            /* B                                            */
-  int32_t n_blocks;         /* nb = ceil(N / B)                             */
+  int32_t n_q_blocks;       /* nb = ceil(N / B)                             */
   int32_t frame_tokens;     /* P >= B                                       */
   const int32_t* row_ptr;   /* device, [nb + 1], as in lvsa_block_mask      */
   const uint32_t* entry;    /* device, [row_ptr[nb]] entry words, kb ascending */
-  const int32_t* pair_ptr;  /* device, [ceil(nb / 2) + 1 + LVSA_PAIR_WORK]  */
-  const uint32_t* pair_word;/* device, token-exact pair words               */
 } lvsa_exact_mask;
 
 /* Host builder of the token-exact form: the handle of lvsa_build_mask
@@ -285,29 +263,22 @@ lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
                              const uint32_t** entry);
 
 /* Device view of the token-exact form of an uploaded handle built by
- * lvsa_build_exact_mask (lvsa_csr_upload copies the entry words and the
- * token-exact pair words too).
+ * lvsa_build_exact_mask (lvsa_csr_upload copies the entry words too).
  * Errors: EINVAL if never uploaded, EUNSUPPORTED as for lvsa_csr_entries. */
 lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out);
 
-/* Device builder of the token-exact form: row_ptr, entry words and the
- * token-exact pair schedule of the same mask as lvsa_build_mask_device, on
- * `stream`, into caller-owned buffers
+/* Device builder of the token-exact form: row_ptr and entry words of the
+ * same mask as lvsa_build_mask_device, on `stream`, into caller-owned
+ * buffers
  *   d_row_ptr    device int32[nb + 1]
  *   d_entry      device uint32[entry_capacity], entry_capacity >= nb * nb
- *   d_pair_ptr   device int32[ceil(nb / 2) + 1 + LVSA_PAIR_WORK], as for
- *                lvsa_build_mask_device
- *   d_pair_word  device uint32[pair_capacity], pair_capacity >=
- *                ceil(nb / 2) * nb; token-exact pair words
  * Errors: EINVAL (ranges, nulls, capacity), EUNSUPPORTED (P < B, B > 255,
  * nb > 65536, or as for lvsa_build_mask_device), EDEVICE (launch). */
 lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
                                          int32_t step, int32_t layer,
                                          const lvsa_params* p,
                                          int32_t* d_row_ptr, uint32_t* d_entry,
-                                         int64_t entry_capacity, int32_t* d_pair_ptr,
-                                         uint32_t* d_pair_word, int64_t pair_capacity,
-                                         void* stream);
+                                         int64_t entry_capacity, void* stream);
 
 /* --------------------------------------------------------- attention ---- */
 
@@ -324,26 +295,38 @@ typedef struct lvsa_tensor {
   int64_t stride_token;
 } lvsa_tensor;
 
-/* Block-sparse attention forward (Eq. 2 over the kept blocks of `mask`, read
- * from its pair schedule):
+/* Tile counters.  The attention kernels run one persistent workgroup per
+ * compute unit; workgroups take tiles (a head and two adjacent query blocks)
+ * through atomic counters, eight per launch (one per XCD), so XCDs that
+ * clock faster take on more tiles.  Every launch gets counters of its own
+ * from a per-device pool the library owns (a few KB, allocated on the first
+ * launch on a device and grown when every counter set is still in use), zeroed
+ * by a small kernel on the launch stream before the attention kernel runs and
+ * handed to a later launch only after an event recorded behind this one has
+ * completed.  A launch recorded into a graph under stream capture keeps its
+ * counters for the life of the process (replays of one graph are ordered).
+ * So nothing that a launch reads is written by another launch: masks and
+ * inputs may be shared by launches in flight on any streams. */
+
+/* Block-sparse attention forward (Eq. 2 over the kept blocks of `mask`):
  *   out[h, i] = sum_j softmax_j(q[h,i] . k[h,j] / sqrt(d)) v[h,j]
  * with j over the real tokens (j < N) of the key blocks kept for the query
  * block of i.  bf16 inputs, fp32 products and softmax, bf16 output (round to
  * nearest even).  q, k, v, out share heads, n_tokens = mask->n_tokens and
- * head_dim = 128; mask->block is 64 or 128.  Rows i >= N of `out` are never
- * written.  out must not overlap q, k or v.  The result is deterministic
- * (fixed key order per row, whichever workgroup computes it).  Launches
- * that share mask->pair_ptr must not overlap in time (its work words, see
- * the pair schedule).
- * Errors: EINVAL (nulls, including the pair schedule, shape mismatch),
- * EUNSUPPORTED (head_dim, block, alignment), EDEVICE (launch). */
+ * head_dim = 128; mask->block is 64 or 128 and mask->n_q_blocks =
+ * mask->n_kv_blocks = ceil(N / B).  Rows i >= N of `out` are never written;
+ * a query block whose row is empty gets zeros.  out must not overlap q, k or
+ * v.  The result is deterministic (fixed key order per row, whichever
+ * workgroup computes it).
+ * Errors: EINVAL (nulls, shape mismatch), EUNSUPPORTED (head_dim, block,
+ * alignment), ENOMEM (tile counters), EDEVICE (launch). */
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream);
 
 /* Token-exact attention forward (Eq. 2 token for token): as lvsa_attention,
  * with the keys of each kept block further restricted, per query token, by
- * the block's pattern (from the token-exact pair words), so query i attends exactly the keys j with
+ * the block's entry word, so query i attends exactly the keys j with
  * frame(j) in A(frame(i)).  mask->block is 64 or 128 and mask->frame_tokens
  * >= mask->block; every query token keeps at least its own frame's keys.
  * Errors as for lvsa_attention. */

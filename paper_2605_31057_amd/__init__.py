@@ -14,16 +14,18 @@ fallback.
     ex = lvsa.build_mask(T=121, P=1560, B=128, step=10, params=p, exact=True)
     ex.upload()
     lvsa.attention_exact(q, k, v, ex.exact_mask(), out)  # Eq. 2 token for token
+    m = lvsa.csr_mask(row_ptr, col_idx, n_tokens, block)  # any block CSR on the device
+    lvsa.attention(q, k, v, m, out)
 """
 import ctypes
 import os
 
 __all__ = [
     "LvsaError", "Params", "Csr", "BlockMask", "ExactMask", "lib",
-    "params_default", "frame_sets", "build_mask", "build_mask_device",
-    "build_exact_mask_device", "attention", "attention_exact",
+    "params_default", "frame_sets", "frame_window", "build_mask", "build_mask_device",
+    "build_exact_mask_device", "csr_mask", "attention", "attention_exact",
     "dense_attention", "WINDOW_BASIC", "WINDOW_ADAPTIVE", "WINDOW_EXPANDED",
-    "MAX_FRAMES", "PAIR_WORK",
+    "MAX_FRAMES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -31,7 +33,6 @@ LIB_PATH = os.path.join(_HERE, "liblvsa.so")
 
 WINDOW_BASIC, WINDOW_ADAPTIVE, WINDOW_EXPANDED = 0, 1, 2
 MAX_FRAMES = 4096
-PAIR_WORK = 16   # LVSA_PAIR_WORK: work words after a device pair_ptr's offsets
 OK, EINVAL, ENOMEM, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
 
 _i32 = ctypes.c_int32
@@ -63,17 +64,16 @@ class Params(ctypes.Structure):
 
 
 class BlockMask(ctypes.Structure):
-    """lvsa_block_mask: device-resident block CSR and its pair schedule."""
-    _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_blocks", _i32),
-                ("row_ptr", _p), ("col_idx", _p), ("pair_ptr", _p), ("pair_word", _p)]
+    """lvsa_block_mask: a block CSR in device memory."""
+    _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_q_blocks", _i32),
+                ("n_kv_blocks", _i32), ("row_ptr", _p), ("col_idx", _p)]
 
 
 class ExactMask(ctypes.Structure):
-    """lvsa_exact_mask: device-resident token-exact form (row_ptr, entry
-    words and the token-exact pair schedule)."""
-    _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_blocks", _i32),
-                ("frame_tokens", _i32), ("row_ptr", _p), ("entry", _p),
-                ("pair_ptr", _p), ("pair_word", _p)]
+    """lvsa_exact_mask: device-resident token-exact form (row_ptr and entry
+    words)."""
+    _fields_ = [("n_tokens", _i32), ("block", _i32), ("n_q_blocks", _i32),
+                ("frame_tokens", _i32), ("row_ptr", _p), ("entry", _p)]
 
 
 class _Tensor(ctypes.Structure):
@@ -99,22 +99,19 @@ def lib():
             "lvsa_version": (_i32, []),
             "lvsa_params_default": (None, [ctypes.POINTER(Params)]),
             "lvsa_frame_sets": (_i32, [_i32, _i32, ctypes.POINTER(Params), _pi32,
-                                       _pi32, _pi32, _pi32, _pi32]),
+                                       _pi32, _pi32, _pi32, _pi32, _pi32]),
+            "lvsa_frame_window": (_i32, [_i32, _i32, ctypes.POINTER(Params), _i32,
+                                         _pi32, _pi32, _pi32]),
             "lvsa_build_mask": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                        ctypes.POINTER(Params), ctypes.POINTER(_p)]),
-            "lvsa_csr_info": (_i32, [_p, _pi32, _pi32, _pi32,
-                                     ctypes.POINTER(_i64), ctypes.POINTER(_pi32),
-                                     ctypes.POINTER(_pi32)]),
+            "lvsa_csr_info": (_i32, [_p, _pi32, _pi32, ctypes.POINTER(_i64),
+                                     ctypes.POINTER(_pi32), ctypes.POINTER(_pi32)]),
+            "lvsa_csr_shape": (_i32, [_p, _pi32, _pi32]),
             "lvsa_csr_upload": (_i32, [_p, _p]),
             "lvsa_csr_free": (None, [_p]),
             "lvsa_csr_device_view": (_i32, [_p, ctypes.POINTER(BlockMask)]),
             "lvsa_build_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
-                                              ctypes.POINTER(Params), _p, _p,
-                                              _i64, _p, _p, _i64, _p]),
-            "lvsa_csr_pairs": (_i32, [_p, _pi32, ctypes.POINTER(_i64),
-                                      ctypes.POINTER(_pi32),
-                                      ctypes.POINTER(ctypes.POINTER(ctypes.c_uint32)),
-                                      ctypes.POINTER(ctypes.POINTER(ctypes.c_uint32))]),
+                                              ctypes.POINTER(Params), _p, _p, _i64, _p]),
             "lvsa_build_exact_mask": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                              ctypes.POINTER(Params),
                                              ctypes.POINTER(_p)]),
@@ -123,7 +120,7 @@ def lib():
             "lvsa_csr_exact_view": (_i32, [_p, ctypes.POINTER(ExactMask)]),
             "lvsa_build_exact_mask_device": (_i32, [_i32, _i32, _i32, _i32, _i32,
                                                     ctypes.POINTER(Params), _p, _p,
-                                                    _i64, _p, _p, _i64, _p]),
+                                                    _i64, _p]),
             "lvsa_attention_exact": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
                                      [ctypes.POINTER(ExactMask),
                                       ctypes.POINTER(_Tensor), _p]),
@@ -151,16 +148,28 @@ def params_default():
     return p
 
 
-def frame_sets(T, step, params=None):
-    """(T_per, anchors, win_lo, win_hi) for one step (lists of ints)."""
+def frame_sets(T, step, params=None, growth=False):
+    """(T_per, anchors, win_lo, win_hi) for one step (lists of ints), plus the
+    Alg. 1 growth steps per frame when ``growth`` is set."""
     params = params or Params()
     tper, n = _i32(), _i32()
     anchors = (_i32 * T)()
     lo = (_i32 * T)()
     hi = (_i32 * T)()
+    grow = (_i32 * T)()
     _check(lib().lvsa_frame_sets(T, step, ctypes.byref(params), ctypes.byref(tper),
-                                 anchors, ctypes.byref(n), lo, hi), "lvsa_frame_sets")
-    return tper.value, list(anchors[:n.value]), list(lo), list(hi)
+                                 anchors, ctypes.byref(n), lo, hi, grow), "lvsa_frame_sets")
+    res = (tper.value, list(anchors[:n.value]), list(lo), list(hi))
+    return res + (list(grow),) if growth else res
+
+
+def frame_window(T, step, t, params=None):
+    """(lo, hi, growth) of query frame t (lvsa_frame_window)."""
+    params = params or Params()
+    lo, hi, g = _i32(), _i32(), _i32()
+    _check(lib().lvsa_frame_window(T, step, ctypes.byref(params), t, ctypes.byref(lo),
+                                   ctypes.byref(hi), ctypes.byref(g)), "lvsa_frame_window")
+    return lo.value, hi.value, g.value
 
 
 def _stream_ptr(stream):
@@ -187,33 +196,42 @@ class Csr:
             self._h = _p()
 
     def info(self):
-        n, b, nb, nnz = _i32(), _i32(), _i32(), _i64()
+        """(n_q_blocks, n_kv_blocks, nnz, row_ptr, col_idx) as lvsa_csr_info
+        returns them (the arrays as ctypes pointers)."""
+        nq, nk, nnz = _i32(), _i32(), _i64()
         rp, ci = _pi32(), _pi32()
-        _check(lib().lvsa_csr_info(self._h, ctypes.byref(n), ctypes.byref(b),
-                                   ctypes.byref(nb), ctypes.byref(nnz),
-                                   ctypes.byref(rp), ctypes.byref(ci)), "lvsa_csr_info")
-        return n.value, b.value, nb.value, nnz.value, rp, ci
+        _check(lib().lvsa_csr_info(self._h, ctypes.byref(nq), ctypes.byref(nk),
+                                   ctypes.byref(nnz), ctypes.byref(rp), ctypes.byref(ci)),
+               "lvsa_csr_info")
+        return nq.value, nk.value, nnz.value, rp, ci
+
+    def shape(self):
+        """(n_tokens, block) of the handle (lvsa_csr_shape)."""
+        n, b = _i32(), _i32()
+        _check(lib().lvsa_csr_shape(self._h, ctypes.byref(n), ctypes.byref(b)),
+               "lvsa_csr_shape")
+        return n.value, b.value
 
     @property
     def n_tokens(self):
-        return self.info()[0]
+        return self.shape()[0]
 
     @property
     def block(self):
-        return self.info()[1]
+        return self.shape()[1]
 
     @property
     def n_blocks(self):
-        return self.info()[2]
+        return self.info()[0]
 
     @property
     def nnz(self):
-        return self.info()[3]
+        return self.info()[2]
 
     def arrays(self):
         """(row_ptr, col_idx) as numpy int32 copies."""
         import numpy as np
-        _, _, nb, nnz, rp, ci = self.info()
+        nb, _, nnz, rp, ci = self.info()
         row_ptr = np.ctypeslib.as_array(rp, shape=(nb + 1,)).copy()
         col_idx = (np.ctypeslib.as_array(ci, shape=(nnz,)).copy() if nnz
                    else np.zeros(0, dtype=np.int32))
@@ -230,27 +248,6 @@ class Csr:
                "lvsa_csr_entries")
         return (np.ctypeslib.as_array(e, shape=(nnz,)).copy() if nnz
                 else np.zeros(0, dtype=np.uint32))
-
-    def pairs(self):
-        """Pair schedule (pair_ptr, block-form words, token-exact words or
-        None) as numpy copies (lvsa_csr_pairs)."""
-        import numpy as np
-        npairs, nw = _i32(), _i64()
-        pp = _pi32()
-        pw = ctypes.POINTER(ctypes.c_uint32)()
-        pe = ctypes.POINTER(ctypes.c_uint32)()
-        _check(lib().lvsa_csr_pairs(self._h, ctypes.byref(npairs), ctypes.byref(nw),
-                                    ctypes.byref(pp), ctypes.byref(pw), ctypes.byref(pe)),
-               "lvsa_csr_pairs")
-        ptr = np.ctypeslib.as_array(pp, shape=(npairs.value + 1,)).copy()
-        n = nw.value
-        words = (np.ctypeslib.as_array(pw, shape=(n,)).copy() if n
-                 else np.zeros(0, dtype=np.uint32))
-        exact = None
-        if pe:
-            exact = (np.ctypeslib.as_array(pe, shape=(n,)).copy() if n
-                     else np.zeros(0, dtype=np.uint32))
-        return ptr, words, exact
 
     def upload(self, stream=None):
         _check(lib().lvsa_csr_upload(self._h, _stream_ptr(stream)), "lvsa_csr_upload")
@@ -280,80 +277,58 @@ def build_mask(T, P, B, step, params=None, layer=0, exact=False):
     return Csr(h.value)
 
 
-def pair_buffers(n_tokens, block, device=None, stream=None):
-    """Device int32 tensors (pair_ptr [ceil(nb/2)+1+PAIR_WORK]: the offsets and
-    the attention kernels' work words; pair words [ceil(nb/2)*nb]) sized for a
-    device builder's pair schedule, allocated on
-    `stream` (a torch stream, a raw stream handle or None for the current
-    one) so the caching allocator reuses them only after that stream's work."""
-    import torch
-    nb = (n_tokens + block - 1) // block
-    npairs = (nb + 1) // 2
-    dev = device or "cuda"
-    if stream is None:
-        s = torch.cuda.current_stream()
-    elif isinstance(stream, int):
-        s = torch.cuda.ExternalStream(stream)
-    else:
-        s = stream
-    with torch.cuda.stream(s):
-        return (torch.empty(npairs + 1 + PAIR_WORK, dtype=torch.int32, device=dev),
-                torch.empty(max(npairs * nb, 1), dtype=torch.int32, device=dev))
-
-
-def _check_pair_ptr(pair_ptr, N, B):
-    npairs = ((N + B - 1) // B + 1) // 2
-    if pair_ptr.numel() < npairs + 1 + PAIR_WORK:
-        raise LvsaError(EINVAL, f"pair_ptr holds {pair_ptr.numel()} words, the pair schedule "
-                        f"needs ceil(nb/2) + 1 + PAIR_WORK = {npairs + 1 + PAIR_WORK}")
-
-
-def _mask_with_pairs(mask, tensors):
+def _mask_keep(mask, tensors):
     mask._keep = tensors   # keep the device buffers alive with the view
     return mask
 
 
 def build_mask_device(T, P, B, step, row_ptr, col_idx, params=None, layer=0,
-                      stream=None, pair_ptr=None, pair_word=None):
-    """Device LVSA mask builder into int32 device tensors (the CSR and its
-    pair schedule; pair buffers are allocated when not given); returns a
-    BlockMask."""
+                      stream=None):
+    """Device LVSA mask builder into int32 device tensors row_ptr [nb+1] and
+    col_idx [>= nb*nb]; returns a BlockMask over them."""
     params = params or Params()
-    N = T * P + params.text_tokens
-    if pair_ptr is None or pair_word is None:
-        pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
-    _check_pair_ptr(pair_ptr, N, B)
     _check(lib().lvsa_build_mask_device(T, P, B, step, layer, ctypes.byref(params),
                                         _p(row_ptr.data_ptr()), _p(col_idx.data_ptr()),
-                                        col_idx.numel(), _p(pair_ptr.data_ptr()),
-                                        _p(pair_word.data_ptr()), pair_word.numel(),
-                                        _stream_ptr(stream)),
+                                        col_idx.numel(), _stream_ptr(stream)),
            "lvsa_build_mask_device")
+    N = T * P + params.text_tokens
     nb = (N + B - 1) // B
-    m = BlockMask(N, B, nb, row_ptr.data_ptr(), col_idx.data_ptr(), pair_ptr.data_ptr(),
-                  pair_word.data_ptr())
-    return _mask_with_pairs(m, (row_ptr, col_idx, pair_ptr, pair_word))
+    m = BlockMask(N, B, nb, nb, row_ptr.data_ptr(), col_idx.data_ptr())
+    return _mask_keep(m, (row_ptr, col_idx))
 
 
 def build_exact_mask_device(T, P, B, step, row_ptr, entry, params=None, layer=0,
-                            stream=None, pair_ptr=None, pair_word=None):
+                            stream=None):
     """Device builder of the token-exact form into device tensors (row_ptr
-    int32 [nb+1], entry int32/uint32 [>= nb*nb], and the token-exact pair
-    schedule, allocated when not given); returns an ExactMask."""
+    int32 [nb+1], entry int32/uint32 [>= nb*nb]); returns an ExactMask."""
     params = params or Params()
-    N = T * P + params.text_tokens
-    if pair_ptr is None or pair_word is None:
-        pair_ptr, pair_word = pair_buffers(N, B, row_ptr.device, stream)
-    _check_pair_ptr(pair_ptr, N, B)
     _check(lib().lvsa_build_exact_mask_device(
         T, P, B, step, layer, ctypes.byref(params), _p(row_ptr.data_ptr()),
-        _p(entry.data_ptr()), entry.numel(), _p(pair_ptr.data_ptr()),
-        _p(pair_word.data_ptr()), pair_word.numel(), _stream_ptr(stream)),
+        _p(entry.data_ptr()), entry.numel(), _stream_ptr(stream)),
         "lvsa_build_exact_mask_device")
+    N = T * P + params.text_tokens
     nb = (N + B - 1) // B
-    m = ExactMask(N, B, nb, P, row_ptr.data_ptr(), entry.data_ptr(), pair_ptr.data_ptr(),
-                  pair_word.data_ptr())
-    return _mask_with_pairs(m, (row_ptr, entry, pair_ptr, pair_word))
+    m = ExactMask(N, B, nb, P, row_ptr.data_ptr(), entry.data_ptr())
+    return _mask_keep(m, (row_ptr, entry))
+
+
+def csr_mask(row_ptr, col_idx, n_tokens, block):
+    """A BlockMask over a caller-built block CSR in device int32 tensors
+    (row_ptr [nb+1], col_idx [nnz], nb = ceil(n_tokens / block))."""
+    nb = (n_tokens + block - 1) // block
+    if row_ptr.numel() != nb + 1:
+        raise LvsaError(EINVAL, f"row_ptr holds {row_ptr.numel()} offsets, the mask has "
+                        f"{nb} query blocks")
+    m = BlockMask(n_tokens, block, nb, nb, row_ptr.data_ptr(), col_idx.data_ptr())
+    return _mask_keep(m, (row_ptr, col_idx))
+
+
+def exact_csr_mask(row_ptr, entry, n_tokens, block, frame_tokens):
+    """An ExactMask over caller-built token-exact entry words in device
+    tensors (row_ptr int32 [nb+1], entry int32/uint32 [nnz])."""
+    nb = (n_tokens + block - 1) // block
+    m = ExactMask(n_tokens, block, nb, frame_tokens, row_ptr.data_ptr(), entry.data_ptr())
+    return _mask_keep(m, (row_ptr, entry))
 
 
 def _tensor(t):

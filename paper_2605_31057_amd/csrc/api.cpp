@@ -1,6 +1,7 @@
 // api.cpp -- the C ABI declared in include/lvsa.h: argument checks, handle
 // management and dispatch to the builders and kernels.
 #include <climits>
+#include <mutex>
 #include <new>
 
 #include "internal.h"
@@ -33,14 +34,15 @@ lvsa_status resolve_frames(int32_t T, int32_t step, const lvsa_params* p,
   c.W = p->window;
   c.tper = tper;
   c.k = ceil_div(T, tper);
-  c.s0 = p->rotate ? step % tper : 0;
+  // Eq. 3 reduces s mod T_per, then every anchor mod T (only the first
+  // reduction matters when T_per <= T).
+  c.s0 = p->rotate ? (step % tper) % T : 0;
   c.mode = p->window_mode;
   c.rotate = p->rotate;
   c.tie_high = p->tie_high;
   c.extra = p->extra_anchors;
   c.text = p->text_tokens;
-  c.g = 0;
-  for (int32_t f = 0; f < T; ++f) c.g += is_anchor(c, f) ? 1 : 0;
+  c.g = anchors_below(c, T);
   *out = c;
   return LVSA_OK;
 }
@@ -54,6 +56,115 @@ lvsa_status check_mask_shape(int32_t T, int32_t P, int32_t B, int32_t L) {
   return LVSA_OK;
 }
 
+// Tile-counter pool (lvsa.h, "Tile counters").  Per device: sets of
+// kTileCounters 64-bit words in chunks of device memory.  An eager launch
+// takes a set whose event (recorded behind the set's last launch) has
+// completed; a launch under stream capture takes a set no launch has used
+// and keeps it, because the graph replays it later (no event can be queried
+// or recorded during a capture).  Sets are zeroed on the launch stream by
+// the attention launch itself, so their contents never matter here.
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int32_t kChunkSets = 256;   // 16 KB per chunk
+
+struct CounterSet {
+  uint64_t* counters = nullptr;
+  hipEvent_t done = nullptr;   // created on the first eager release
+  bool busy = false;           // between acquire and release
+  bool kept = false;           // recorded into a graph: never handed out again
+  bool used = false;           // handed out at least once
+};
+
+struct CounterPool {
+  std::mutex mu;
+  std::vector<CounterSet> sets;
+  int32_t next = 0;
+};
+
+CounterPool g_pools[kMaxDevices];
+
+lvsa_status grow_pool(CounterPool& pool) {
+  void* chunk = nullptr;
+  if (hipMalloc(&chunk, sizeof(uint64_t) * kTileCounters * kChunkSets) != hipSuccess)
+    return LVSA_ENOMEM;
+  for (int32_t i = 0; i < kChunkSets; ++i) {
+    CounterSet cs;
+    cs.counters = (uint64_t*)chunk + (size_t)kTileCounters * i;
+    pool.sets.push_back(cs);
+  }
+  return LVSA_OK;
+}
+
+}  // namespace
+
+lvsa_status acquire_counters(hipStream_t stream, CounterLease* lease) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LVSA_EDEVICE;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cap) != hipSuccess) return LVSA_EDEVICE;
+  const bool capturing = cap != hipStreamCaptureStatusNone;
+  CounterPool& pool = g_pools[dev];
+  std::lock_guard<std::mutex> lock(pool.mu);
+  try {
+    if (pool.sets.empty()) {
+      const lvsa_status st = grow_pool(pool);
+      if (st != LVSA_OK) return st;
+    }
+    const int32_t n = (int32_t)pool.sets.size();
+    int32_t pick = -1;
+    for (int32_t d = 0; d < n && pick < 0; ++d) {
+      const int32_t i = (pool.next + d) % n;
+      CounterSet& cs = pool.sets[i];
+      if (cs.busy || cs.kept) continue;
+      if (capturing) {
+        if (!cs.used) pick = i;
+        continue;
+      }
+      if (cs.done) {
+        const hipError_t q = hipEventQuery(cs.done);
+        if (q == hipErrorNotReady) continue;
+        if (q != hipSuccess) return LVSA_EDEVICE;
+      }
+      pick = i;
+    }
+    if (pick < 0) {
+      const lvsa_status st = grow_pool(pool);
+      if (st != LVSA_OK) return st;
+      pick = n;
+    }
+    CounterSet& cs = pool.sets[pick];
+    cs.busy = true;
+    cs.used = true;
+    pool.next = (pick + 1) % (int32_t)pool.sets.size();
+    lease->device = dev;
+    lease->slot = pick;
+    lease->counters = cs.counters;
+    lease->captured = capturing;
+  } catch (const std::bad_alloc&) {
+    return LVSA_ENOMEM;
+  }
+  return LVSA_OK;
+}
+
+void release_counters(const CounterLease& lease, hipStream_t stream) {
+  if (lease.slot < 0) return;
+  CounterPool& pool = g_pools[lease.device];
+  std::lock_guard<std::mutex> lock(pool.mu);
+  CounterSet& cs = pool.sets[lease.slot];
+  cs.busy = false;
+  if (lease.captured) {
+    cs.kept = true;
+    return;
+  }
+  if (!cs.done && hipEventCreateWithFlags(&cs.done, hipEventDisableTiming) != hipSuccess) {
+    cs.done = nullptr;
+    cs.kept = true;   // no way to know when the launch ends: never reuse it
+    return;
+  }
+  if (hipEventRecord(cs.done, stream) != hipSuccess) cs.kept = true;
+}
+
 }  // namespace lvsa
 
 struct lvsa_csr {
@@ -65,32 +176,24 @@ struct lvsa_csr {
   std::vector<int32_t> row_ptr;
   std::vector<int32_t> col_idx;
   std::vector<uint32_t> entry;
-  std::vector<int32_t> pair_ptr;   // pair schedule (block words, and
-  std::vector<uint32_t> pair_word; // token-exact words with entry words)
-  std::vector<uint32_t> pair_exact;
-  // Device copies, in one allocation each, sized when first uploaded.
+  // Device copies, allocated in stream order on the first upload.
   int32_t* d_row_ptr = nullptr;
   int32_t* d_col_idx = nullptr;
   uint32_t* d_entry = nullptr;
-  int32_t* d_pair_ptr = nullptr;
-  uint32_t* d_pair_word = nullptr;
-  uint32_t* d_pair_exact = nullptr;
+  hipStream_t upload_stream = nullptr;   // stream of the last upload
+  hipEvent_t uploaded = nullptr;         // recorded behind the last upload
 };
 
 namespace {
 
-// Device copy of a host array: allocated on the first upload (the handle's
-// arrays never change size), then copied asynchronously on `s`.
-// Device copy of `host` followed by `zeros` zero elements (allocated on the
-// first upload, reused after).
+// Device copy of a host array: allocated in the order of `s` on the first
+// upload (the handle's arrays never change size), then copied asynchronously
+// on `s`.
 template <typename T>
-lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s,
-                         size_t zeros = 0) {
-  static const T kZeros[LVSA_PAIR_WORK] = {};
-  if (zeros > LVSA_PAIR_WORK) return LVSA_EINVAL;
+lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s) {
   if (!*dev) {
-    const size_t n = (host.empty() ? 1 : host.size()) + zeros;
-    if (hipMalloc(dev, sizeof(T) * n) != hipSuccess) {
+    const size_t n = host.empty() ? 1 : host.size();
+    if (hipMallocAsync((void**)dev, sizeof(T) * n, s) != hipSuccess) {
       *dev = nullptr;
       return LVSA_ENOMEM;
     }
@@ -98,9 +201,6 @@ lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s,
   if (!host.empty() &&
       hipMemcpyAsync(*dev, host.data(), sizeof(T) * host.size(), hipMemcpyHostToDevice,
                      s) != hipSuccess)
-    return LVSA_EDEVICE;
-  if (zeros && hipMemcpyAsync(*dev + host.size(), kZeros, sizeof(T) * zeros,
-                              hipMemcpyHostToDevice, s) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -122,7 +222,7 @@ const char* lvsa_status_str(lvsa_status s) {
   }
 }
 
-int32_t lvsa_version(void) { return 10500; }
+int32_t lvsa_version(void) { return 20000; }
 
 void lvsa_params_default(lvsa_params* p) {
   if (!p) return;
@@ -139,7 +239,7 @@ void lvsa_params_default(lvsa_params* p) {
 lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
                             int32_t* tper_out, int32_t* anchors,
                             int32_t* n_anchors, int32_t* win_lo,
-                            int32_t* win_hi) {
+                            int32_t* win_hi, int32_t* growth) {
   FrameCfg c;
   const lvsa_status st = resolve_frames(T, step, p, &c);
   if (st != LVSA_OK) return st;
@@ -153,10 +253,26 @@ lvsa_status lvsa_frame_sets(int32_t T, int32_t step, const lvsa_params* p,
   if (n_anchors) *n_anchors = n;
   for (int32_t t = 0; t < T; ++t) {
     int32_t lo, hi;
-    frame_window(c, t, &lo, &hi);
+    const int32_t g = frame_window(c, t, &lo, &hi);
     if (win_lo) win_lo[t] = lo;
     if (win_hi) win_hi[t] = hi;
+    if (growth) growth[t] = g;
   }
+  return LVSA_OK;
+}
+
+lvsa_status lvsa_frame_window(int32_t T, int32_t step, const lvsa_params* p,
+                              int32_t t, int32_t* lo, int32_t* hi,
+                              int32_t* growth) {
+  FrameCfg c;
+  const lvsa_status st = resolve_frames(T, step, p, &c);
+  if (st != LVSA_OK) return st;
+  if (t < 0 || t >= T) return LVSA_EINVAL;
+  int32_t l, h;
+  const int32_t g = frame_window(c, t, &l, &h);
+  if (lo) *lo = l;
+  if (hi) *hi = h;
+  if (growth) *growth = g;
   return LVSA_OK;
 }
 
@@ -179,10 +295,7 @@ lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
   if (!h) return LVSA_ENOMEM;
   h->has_entry = exact;
   try {
-    build_csr_host(c, P, B, &h->row_ptr, &h->col_idx,
-                   h->has_entry ? &h->entry : nullptr);
-    build_pairs_host(h->row_ptr, h->col_idx, h->has_entry ? &h->entry : nullptr,
-                     &h->pair_ptr, &h->pair_word, h->has_entry ? &h->pair_exact : nullptr);
+    build_csr_host(c, P, B, &h->row_ptr, &h->col_idx, h->has_entry ? &h->entry : nullptr);
   } catch (const std::bad_alloc&) {
     delete h;
     return LVSA_ENOMEM;
@@ -209,72 +322,66 @@ lvsa_status lvsa_build_exact_mask(int32_t T, int32_t P, int32_t B,
   return build_mask_handle(T, P, B, step, layer, p, true, out);
 }
 
-lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_tokens,
-                          int32_t* block, int32_t* n_blocks, int64_t* nnz,
+lvsa_status lvsa_csr_info(const lvsa_csr* csr, int32_t* n_q_blocks,
+                          int32_t* n_kv_blocks, int64_t* nnz,
                           const int32_t** row_ptr, const int32_t** col_idx) {
   if (!csr) return LVSA_EINVAL;
-  if (n_tokens) *n_tokens = csr->n_tokens;
-  if (block) *block = csr->block;
-  if (n_blocks) *n_blocks = csr->n_blocks;
+  if (n_q_blocks) *n_q_blocks = csr->n_blocks;
+  if (n_kv_blocks) *n_kv_blocks = csr->n_blocks;
   if (nnz) *nnz = (int64_t)csr->col_idx.size();
   if (row_ptr) *row_ptr = csr->row_ptr.data();
   if (col_idx) *col_idx = csr->col_idx.data();
   return LVSA_OK;
 }
 
+lvsa_status lvsa_csr_shape(const lvsa_csr* csr, int32_t* n_tokens, int32_t* block) {
+  if (!csr) return LVSA_EINVAL;
+  if (n_tokens) *n_tokens = csr->n_tokens;
+  if (block) *block = csr->block;
+  return LVSA_OK;
+}
+
 lvsa_status lvsa_csr_upload(lvsa_csr* csr, void* stream) {
   if (!csr) return LVSA_EINVAL;
   hipStream_t s = (hipStream_t)stream;
+  // Device arrays live in the order of the stream they were allocated on;
+  // a later upload on another stream first waits for that one's copies.
+  if (csr->uploaded && s != csr->upload_stream &&
+      hipStreamWaitEvent(s, csr->uploaded, 0) != hipSuccess)
+    return LVSA_EDEVICE;
   lvsa_status st;
   if ((st = upload_array(csr->row_ptr, &csr->d_row_ptr, s)) != LVSA_OK) return st;
   if ((st = upload_array(csr->col_idx, &csr->d_col_idx, s)) != LVSA_OK) return st;
-  if ((st = upload_array(csr->pair_ptr, &csr->d_pair_ptr, s, LVSA_PAIR_WORK)) != LVSA_OK)
+  if (csr->has_entry && (st = upload_array(csr->entry, &csr->d_entry, s)) != LVSA_OK)
     return st;
-  if ((st = upload_array(csr->pair_word, &csr->d_pair_word, s)) != LVSA_OK) return st;
-  if (csr->has_entry) {
-    if ((st = upload_array(csr->entry, &csr->d_entry, s)) != LVSA_OK) return st;
-    if ((st = upload_array(csr->pair_exact, &csr->d_pair_exact, s)) != LVSA_OK) return st;
+  if (!csr->uploaded &&
+      hipEventCreateWithFlags(&csr->uploaded, hipEventDisableTiming) != hipSuccess) {
+    csr->uploaded = nullptr;
+    return LVSA_EDEVICE;
   }
+  if (hipEventRecord(csr->uploaded, s) != hipSuccess) return LVSA_EDEVICE;
+  csr->upload_stream = s;
   return LVSA_OK;
 }
 
 void lvsa_csr_free(lvsa_csr* csr) {
   if (!csr) return;
-  void* dev[] = {csr->d_row_ptr, csr->d_col_idx, csr->d_entry,
-                 csr->d_pair_ptr, csr->d_pair_word, csr->d_pair_exact};
-  bool any = false;
-  for (void* d : dev) any = any || d != nullptr;
-  if (any) {
-    (void)hipDeviceSynchronize();
-    for (void* d : dev)
-      if (d) (void)hipFree(d);
-  }
+  // The host arrays are the source of the last upload's copies.
+  if (csr->uploaded) (void)hipEventSynchronize(csr->uploaded);
+  for (void* d : {(void*)csr->d_row_ptr, (void*)csr->d_col_idx, (void*)csr->d_entry})
+    if (d) (void)hipFreeAsync(d, csr->upload_stream);
+  if (csr->uploaded) (void)hipEventDestroy(csr->uploaded);
   delete csr;
 }
 
-lvsa_status lvsa_csr_pairs(const lvsa_csr* csr, int32_t* n_pairs, int64_t* n_words,
-                           const int32_t** pair_ptr, const uint32_t** pair_word,
-                           const uint32_t** pair_exact) {
-  if (!csr) return LVSA_EINVAL;
-  if (n_pairs) *n_pairs = (int32_t)csr->pair_ptr.size() - 1;
-  if (n_words) *n_words = (int64_t)csr->pair_word.size();
-  if (pair_ptr) *pair_ptr = csr->pair_ptr.data();
-  if (pair_word) *pair_word = csr->pair_word.data();
-  if (pair_exact) *pair_exact = csr->has_entry ? csr->pair_exact.data() : nullptr;
-  return LVSA_OK;
-}
-
 lvsa_status lvsa_csr_device_view(const lvsa_csr* csr, lvsa_block_mask* out) {
-  if (!csr || !out || !csr->d_row_ptr || !csr->d_col_idx || !csr->d_pair_ptr ||
-      !csr->d_pair_word)
-    return LVSA_EINVAL;
+  if (!csr || !out || !csr->d_row_ptr || !csr->d_col_idx) return LVSA_EINVAL;
   out->n_tokens = csr->n_tokens;
   out->block = csr->block;
-  out->n_blocks = csr->n_blocks;
+  out->n_q_blocks = csr->n_blocks;
+  out->n_kv_blocks = csr->n_blocks;
   out->row_ptr = csr->d_row_ptr;
   out->col_idx = csr->d_col_idx;
-  out->pair_ptr = csr->d_pair_ptr;
-  out->pair_word = csr->d_pair_word;
   return LVSA_OK;
 }
 
@@ -290,16 +397,48 @@ lvsa_status lvsa_csr_entries(const lvsa_csr* csr, int32_t* frame_tokens,
 lvsa_status lvsa_csr_exact_view(const lvsa_csr* csr, lvsa_exact_mask* out) {
   if (!csr || !out) return LVSA_EINVAL;
   if (!csr->has_entry) return LVSA_EUNSUPPORTED;
-  if (!csr->d_row_ptr || !csr->d_entry || !csr->d_pair_ptr || !csr->d_pair_exact)
-    return LVSA_EINVAL;
+  if (!csr->d_row_ptr || !csr->d_entry) return LVSA_EINVAL;
   out->n_tokens = csr->n_tokens;
   out->block = csr->block;
-  out->n_blocks = csr->n_blocks;
+  out->n_q_blocks = csr->n_blocks;
   out->frame_tokens = csr->frame_tokens;
   out->row_ptr = csr->d_row_ptr;
   out->entry = csr->d_entry;
-  out->pair_ptr = csr->d_pair_ptr;
-  out->pair_word = csr->d_pair_exact;
+  return LVSA_OK;
+}
+
+namespace {
+
+// Common checks of the device builders; resolves the frame rules and nb.
+lvsa_status check_device_build(int32_t T, int32_t P, int32_t B, int32_t step,
+                               int32_t layer, const lvsa_params* p, FrameCfg* c,
+                               int64_t* nb) {
+  if (layer < 0) return LVSA_EINVAL;
+  lvsa_status st = resolve_frames(T, step, p, c);
+  if (st != LVSA_OK) return st;
+  st = check_mask_shape(T, P, B, c->text);
+  if (st != LVSA_OK) return st;
+  *nb = (mask_tokens(*c, P) + B - 1) / B;
+  return LVSA_OK;
+}
+
+}  // namespace
+
+lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
+                                   int32_t step, int32_t layer,
+                                   const lvsa_params* p, int32_t* d_row_ptr,
+                                   int32_t* d_col_idx, int64_t col_capacity,
+                                   void* stream) {
+  if (!d_row_ptr || !d_col_idx) return LVSA_EINVAL;
+  FrameCfg c;
+  int64_t nb = 0;
+  const lvsa_status st = check_device_build(T, P, B, step, layer, p, &c, &nb);
+  if (st != LVSA_OK) return st;
+  if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
+  if (col_capacity < nb * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr,
+                               (hipStream_t)stream) != hipSuccess)
+    return LVSA_EDEVICE;
   return LVSA_OK;
 }
 
@@ -307,44 +446,17 @@ lvsa_status lvsa_build_exact_mask_device(int32_t T, int32_t P, int32_t B,
                                          int32_t step, int32_t layer,
                                          const lvsa_params* p,
                                          int32_t* d_row_ptr, uint32_t* d_entry,
-                                         int64_t entry_capacity, int32_t* d_pair_ptr,
-                                         uint32_t* d_pair_word, int64_t pair_capacity,
-                                         void* stream) {
-  if (layer < 0 || !d_row_ptr || !d_entry || !d_pair_ptr || !d_pair_word)
-    return LVSA_EINVAL;
+                                         int64_t entry_capacity, void* stream) {
+  if (!d_row_ptr || !d_entry) return LVSA_EINVAL;
   FrameCfg c;
-  lvsa_status st = resolve_frames(T, step, p, &c);
+  int64_t nb = 0;
+  const lvsa_status st = check_device_build(T, P, B, step, layer, p, &c, &nb);
   if (st != LVSA_OK) return st;
-  st = check_mask_shape(T, P, B, c.text);
-  if (st != LVSA_OK) return st;
-  const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
   if (!exact_supported(P, B, nb)) return LVSA_EUNSUPPORTED;
   if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
-  if (entry_capacity < nb * nb || pair_capacity < (nb + 1) / 2 * nb) return LVSA_EINVAL;
-  if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry, d_pair_ptr,
-                               d_pair_word, true, (hipStream_t)stream) != hipSuccess)
-    return LVSA_EDEVICE;
-  return LVSA_OK;
-}
-
-lvsa_status lvsa_build_mask_device(int32_t T, int32_t P, int32_t B,
-                                   int32_t step, int32_t layer,
-                                   const lvsa_params* p, int32_t* d_row_ptr,
-                                   int32_t* d_col_idx, int64_t col_capacity,
-                                   int32_t* d_pair_ptr, uint32_t* d_pair_word,
-                                   int64_t pair_capacity, void* stream) {
-  if (layer < 0 || !d_row_ptr || !d_col_idx || !d_pair_ptr || !d_pair_word)
-    return LVSA_EINVAL;
-  FrameCfg c;
-  lvsa_status st = resolve_frames(T, step, p, &c);
-  if (st != LVSA_OK) return st;
-  st = check_mask_shape(T, P, B, c.text);
-  if (st != LVSA_OK) return st;
-  const int64_t nb = (mask_tokens(c, P) + B - 1) / B;
-  if (!device_mask_supported(c, P, B)) return LVSA_EUNSUPPORTED;
-  if (col_capacity < nb * nb || pair_capacity < (nb + 1) / 2 * nb) return LVSA_EINVAL;
-  if (launch_build_mask_device(c, P, B, d_row_ptr, d_col_idx, nullptr, d_pair_ptr,
-                               d_pair_word, false, (hipStream_t)stream) != hipSuccess)
+  if (entry_capacity < nb * nb) return LVSA_EINVAL;
+  if (launch_build_mask_device(c, P, B, d_row_ptr, nullptr, d_entry,
+                               (hipStream_t)stream) != hipSuccess)
     return LVSA_EDEVICE;
   return LVSA_OK;
 }
@@ -361,18 +473,16 @@ lvsa_status check_tensor(const lvsa_tensor* t, int32_t heads, int32_t n) {
   return LVSA_OK;
 }
 
-lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
-                          const lvsa_tensor* v, int32_t n_tokens,
-                          int32_t block, int32_t n_blocks,
-                          const int32_t* pair_ptr, const uint32_t* pair_word,
-                          int32_t frame_tokens, AttnMode mode,
-                          lvsa_tensor* out, void* stream) {
+// Checks the tensors against (N, B, nb) and fills the launch arguments
+// except the mask and the counters.
+lvsa_status attention_args(const lvsa_tensor* q, const lvsa_tensor* k,
+                           const lvsa_tensor* v, int32_t n_tokens, int32_t block,
+                           int32_t n_blocks, lvsa_tensor* out, AttnArgs* a) {
   if (!q || !k || !v || !out) return LVSA_EINVAL;
   if (block != 64 && block != 128) return LVSA_EUNSUPPORTED;
   const int32_t H = q->heads;
   if (H < 1 || n_tokens < 1) return LVSA_EINVAL;
-  if (n_blocks != (int32_t)(((int64_t)n_tokens + block - 1) / block))
-    return LVSA_EINVAL;
+  if (n_blocks != (int32_t)(((int64_t)n_tokens + block - 1) / block)) return LVSA_EINVAL;
   // Work-items per launch must stay below 2^32.
   if ((int64_t)n_blocks * H * block * 2 >= ((int64_t)1 << 32)) return LVSA_EUNSUPPORTED;
   lvsa_status st;
@@ -387,27 +497,42 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
     return LVSA_EUNSUPPORTED;
   if (out->data == q->data || out->data == k->data || out->data == v->data)
     return LVSA_EINVAL;
-  AttnArgs a;
-  a.q = q->data;
-  a.k = k->data;
-  a.v = v->data;
-  a.o = out->data;
-  a.q_sh = q->stride_head;
-  a.q_st = q->stride_token;
-  a.k_sh = k->stride_head;
-  a.k_st = k->stride_token;
-  a.v_sh = v->stride_head;
-  a.v_st = v->stride_token;
-  a.o_sh = out->stride_head;
-  a.o_st = out->stride_token;
-  a.heads = H;
-  a.n_tokens = n_tokens;
-  a.n_blocks = n_blocks;
-  a.pair_ptr = pair_ptr;
-  a.pair_word = pair_word;
-  a.frame_tokens = frame_tokens;
-  if (launch_attention(a, block, mode, (hipStream_t)stream) != hipSuccess)
+  a->q = q->data;
+  a->k = k->data;
+  a->v = v->data;
+  a->o = out->data;
+  a->q_sh = q->stride_head;
+  a->q_st = q->stride_token;
+  a->k_sh = k->stride_head;
+  a->k_st = k->stride_token;
+  a->v_sh = v->stride_head;
+  a->v_st = v->stride_token;
+  a->o_sh = out->stride_head;
+  a->o_st = out->stride_token;
+  a->heads = H;
+  a->n_tokens = n_tokens;
+  a->n_blocks = n_blocks;
+  a->row_ptr = nullptr;
+  a->rows = nullptr;
+  a->frame_tokens = 0;
+  a->counters = nullptr;
+  return LVSA_OK;
+}
+
+// Launches with a counter set of the pool (lvsa.h, "Tile counters").
+lvsa_status run_attention(AttnArgs& a, int32_t block, AttnMode mode, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  CounterLease lease;
+  const lvsa_status st = acquire_counters(s, &lease);
+  if (st != LVSA_OK) return st;
+  a.counters = lease.counters;
+  if (launch_attention(a, block, mode, s) != hipSuccess) {
+    CounterLease unused = lease;
+    unused.captured = false;
+    release_counters(unused, s);
     return LVSA_EDEVICE;
+  }
+  release_counters(lease, s);
   return LVSA_OK;
 }
 
@@ -416,22 +541,33 @@ lvsa_status run_attention(const lvsa_tensor* q, const lvsa_tensor* k,
 lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream) {
-  if (!mask || !mask->pair_ptr || !mask->pair_word) return LVSA_EINVAL;
-  return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
-                       mask->pair_ptr, mask->pair_word, 0, ATTN_BLOCK, out, stream);
+  if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
+  if (mask->n_kv_blocks != mask->n_q_blocks) return LVSA_EINVAL;
+  AttnArgs a;
+  const lvsa_status st = attention_args(q, k, v, mask->n_tokens, mask->block,
+                                        mask->n_q_blocks, out, &a);
+  if (st != LVSA_OK) return st;
+  a.row_ptr = mask->row_ptr;
+  a.rows = (const uint32_t*)mask->col_idx;
+  return run_attention(a, mask->block, ATTN_BLOCK, stream);
 }
 
 lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  const lvsa_tensor* v,
                                  const lvsa_exact_mask* mask, lvsa_tensor* out,
                                  void* stream) {
-  if (!mask || !mask->pair_ptr || !mask->pair_word) return LVSA_EINVAL;
+  if (!mask || !mask->row_ptr || !mask->entry) return LVSA_EINVAL;
   if (mask->frame_tokens < 1) return LVSA_EINVAL;
-  if (!exact_supported(mask->frame_tokens, mask->block, mask->n_blocks))
+  if (!exact_supported(mask->frame_tokens, mask->block, mask->n_q_blocks))
     return LVSA_EUNSUPPORTED;
-  return run_attention(q, k, v, mask->n_tokens, mask->block, mask->n_blocks,
-                       mask->pair_ptr, mask->pair_word, mask->frame_tokens, ATTN_EXACT,
-                       out, stream);
+  AttnArgs a;
+  const lvsa_status st = attention_args(q, k, v, mask->n_tokens, mask->block,
+                                        mask->n_q_blocks, out, &a);
+  if (st != LVSA_OK) return st;
+  a.row_ptr = mask->row_ptr;
+  a.rows = mask->entry;
+  a.frame_tokens = mask->frame_tokens;
+  return run_attention(a, mask->block, ATTN_EXACT, stream);
 }
 
 lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
@@ -442,8 +578,10 @@ lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   const int32_t n = q->n_tokens;
   if (n < 1) return LVSA_EINVAL;
   const int32_t nb = (int32_t)(((int64_t)n + block - 1) / block);
-  return run_attention(q, k, v, n, block, nb, nullptr, nullptr, 0, ATTN_DENSE,
-                       out, stream);
+  AttnArgs a;
+  const lvsa_status st = attention_args(q, k, v, n, block, nb, out, &a);
+  if (st != LVSA_OK) return st;
+  return run_attention(a, block, ATTN_DENSE, stream);
 }
 
 }  // extern "C"

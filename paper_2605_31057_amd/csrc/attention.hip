@@ -1,21 +1,31 @@
 // attention.hip -- block-sparse and dense flash-attention forward for gfx950.
 //
 // Computes Eq. 2 of the LVSA paper (softmax attention restricted to a key
-// set) with the key set of every query block given by a block mask (read in
-// its pair-schedule form), and Eq. 1 (all keys) with the same kernel visiting
-// every key block.
+// set) with the key set of every query block given by a block CSR, and Eq. 1
+// (all keys) with the same kernel visiting every key block.
 //
 // Work decomposition
-//   One workgroup per (head, pair of query blocks 2p and 2p+1): 2*BLOCK query
-//   rows, NW = 2*BLOCK/32 waves (8 at BLOCK = 128) of 32 rows each; waves
+//   A tile is (head, pair of query blocks 2p and 2p+1): 2*BLOCK query rows,
+//   NW = 2*BLOCK/32 waves (8 at BLOCK = 128) of 32 rows each; waves
 //   0..NW/2-1 hold rows of query block 2p, the others rows of 2p+1.  The
-//   workgroup walks the pair's schedule (the union of the two blocks' key
-//   lists, each word saying which of the two keeps the key block, lvsa.h) one
-//   key block per step, and every wave takes all BLOCK keys of the step for
-//   its rows.  Adjacent query blocks mostly keep the same key blocks (they
-//   touch the same frames), so each K/V tile brought from HBM/L2 into LDS
-//   serves 2*BLOCK query rows; a key block that only one of the two keeps is
-//   masked out (no valid keys) for the other's waves.
+//   workgroup walks the union of the two blocks' key lists one key block per
+//   step, and every wave takes all BLOCK keys of the step for its rows.
+//   Adjacent query blocks mostly keep the same key blocks (they touch the
+//   same frames), so each K/V tile brought from HBM/L2 into LDS serves
+//   2*BLOCK query rows; a key block that only one of the two keeps is masked
+//   out (no valid keys) for the other's waves.  One persistent workgroup per
+//   compute unit takes tiles through atomic counters (fetch_tile).
+//
+// The merged walk
+//   CSR rows 2p and 2p+1 are walked from their last entries down: each step
+//   takes the larger of the two rows' next entries (both, when they are
+//   equal), so the step's key block comes with a flag per query block and
+//   the key blocks come in descending order, each once.  The merge is scalar
+//   arithmetic, repeated in every wave, on two candidate entries that one
+//   vector load (lanes 0 and 1) fetches at the start of the step whose end
+//   consumes them; merges run three steps ahead of the step that uses their
+//   key block, because K tiles are loaded two steps ahead.  The mask is only
+//   read, so any number of launches can share it.
 //
 // Schedule ("ping-pong", one key block per step)
 //   Waves w and w + NW/2 (which share a SIMD when NW = 8) run half a step
@@ -36,8 +46,8 @@
 //   A whole key block per step keeps the per-step costs (two barriers, the
 //   loop, the load set-up) small against the step's 72 MFMAs per wave; S
 //   (64 registers) and P (32) then fill the register file, so the GEMM
-//   phase finishes P(j) before it produces S(j+1) and the masks avoid
-//   per-element lane masks (comparisons into SGPR pairs).
+//   phase finishes P(j) before it produces S(j+1), and masks run only in a
+//   wave-uniform branch, one compare into VCC and one select per score.
 //
 // Contractions (bf16 MFMA 32x32x16, fp32 accumulate)
 //     S^T = K Q^T     A = K rows (LDS, ds_read_b128), B = Q rows (registers)
@@ -74,16 +84,6 @@ constexpr float RESCALE_SLACK = 8.f;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-__device__ __forceinline__ int xcd_remap(int bid, int total) {
-  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-  // contiguous range of logical tiles so that neighbouring query blocks of a
-  // head, whose key lists overlap, share that XCD's L2.
-  const int per = total / 8, rem = total % 8;
-  const int xcd = bid % 8, idx = bid / 8;
-  return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) +
-         idx;
-}
-
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base,
                                                             uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
@@ -110,14 +110,9 @@ __device__ __forceinline__ float pair_max(float x) {
 constexpr int SLAB_ROW = 64;
 __device__ __forceinline__ int xsw(int row) { return (row >> 2) & 3; }
 
-#ifndef LVSA_QT
-#define LVSA_QT 1
-#endif
-constexpr int QT = LVSA_QT;   // 32-row query tiles per wave
-
 template <int BLOCK>
 struct Tile {
-  static constexpr int NW = 2 * BLOCK / (32 * QT);  // waves (32*QT query rows each)
+  static constexpr int NW = 2 * BLOCK / 32;         // waves (32 query rows each)
   static constexpr int NT = NW * 64;                // threads
   static constexpr int KTW = BLOCK / 32;            // 32-key tiles per step
   static constexpr int SLAB = BLOCK * SLAB_ROW;     // bytes per slab
@@ -128,20 +123,15 @@ struct Tile {
   static_assert(LOADS * NW == INSTR, "tile load mapping");
 };
 
-// Issues the direct-to-LDS loads of rows kb*BLOCK .. +BLOCK-1 of one tensor
-// into the tile at LDS byte address `lds`.  Wave load I fills tile bytes
-// 1024*I .. +1023: slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk
-// lane%4, which holds logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).
-// lane_off = (lane/4)*row_bytes + 16*((lane%4) ^ (lane/16)) is the per-lane
-// part of the global byte offset.  Rows at or past N fall outside the buffer
-// resource and read as zeros.  The loads are issued from inline assembly so
-// the compiler does not track them: they are waited for explicitly (vmcnt(0)
-// plus a barrier) at the end of the step, and no compiler-inserted wait can
-// stall the phases in between.
-// One wave load of a tile into LDS bytes 1024*I ..: `rsrc` starts at the
-// tile's first row, `voff` = per-lane offset + the load's uniform offset.
-// The nop is the wait state gfx9 needs between an SALU write of M0 and an
-// LDS-DMA instruction (the compiler cannot see into the statement to add it).
+// One wave load (1 KiB) of a K or V tile into LDS at byte address lds_dst:
+// `rsrc` starts at the tile's first row, `voff` = the lane's part of the
+// global byte offset plus the load's uniform part (LoadPlan).  Rows at or
+// past N fall outside the buffer resource and read as zeros.  The loads are
+// issued from inline assembly so the compiler does not track them: they are
+// waited for explicitly (vmcnt(0) plus a barrier) at the end of the step, and
+// no compiler-inserted wait can stall the phases in between.  The nop is the
+// wait state gfx9 needs between an SALU write of M0 and an LDS-DMA
+// instruction (the compiler cannot see into the statement to add it).
 __device__ __forceinline__ void issue_load(uint32_t lds_dst, __amdgpu_buffer_rsrc_t rsrc,
                                            uint32_t voff) {
   asm volatile(
@@ -166,11 +156,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const __bf16* head_b
   return make_rsrc(head_base + skip, bytes);
 }
 
-// Per-wave load plan: load j of wave w fills tile bytes 1024*I (I = w + NW*j):
-// slab I / IPS, rows 16*(I % IPS) + lane/4, physical chunk lane%4, which holds
-// logical chunk (lane%4) ^ x(row) = (lane%4) ^ (lane/16).  The per-lane part
-// of the global offset is (lane/4)*row_bytes + 16*((lane%4) ^ (lane/16)); the
-// per-load part is uniform.
 // Per-wave load plan: wave w's load j of a tile fills tile bytes
 // 1024*(w + NW*j): slab j, rows 16*w + lane/4 (NW = IPS: one wave per 16-row
 // band of a slab), physical chunk lane%4, which holds logical chunk
@@ -232,7 +217,7 @@ __device__ __forceinline__ void wait_loads_and_sync() {
 
 template <int BLOCK>
 struct Scores {
-  f32x16 s[QT][Tile<BLOCK>::KTW];   // [q tile][key tile]
+  f32x16 s[Tile<BLOCK>::KTW];   // one 32-key tile each
 };
 
 // Per-lane LDS byte offsets (within a tile) of the K and V fragments.
@@ -266,35 +251,27 @@ __device__ __forceinline__ FragAddr frag_addr(int lane) {
 
 // S^T = K Q^T for the keys of one step (K tile at lds_k).
 template <int BLOCK>
-__device__ __forceinline__ void compute_scores(const char* lds_k,
-                                               const bf16x8 (&qf)[QT][8],
-                                               Scores<BLOCK>& sc,
-                                               const FragAddr& fa) {
+__device__ __forceinline__ void compute_scores(const char* lds_k, const bf16x8 (&qf)[8],
+                                               Scores<BLOCK>& sc, const FragAddr& fa) {
   using TL = Tile<BLOCK>;
 #pragma unroll
   for (int kt = 0; kt < TL::KTW; ++kt) {
-    f32x16 acc[QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) acc[qt] = f32x16{};
+    f32x16 acc = f32x16{};
 #pragma unroll
     for (int stp = 0; stp < 8; ++stp) {
       const uint32_t off = ((stp & 1) ? fa.k_odd : fa.k_even) +
                            (stp / 2) * TL::SLAB + kt * 32 * SLAB_ROW;
       const bf16x8 a = *(const bf16x8*)(lds_k + off);
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-        acc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qt][stp], acc[qt], 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[stp], acc, 0, 0, 0);
     }
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) sc.s[qt][kt] = acc[qt];
+    sc.s[kt] = acc;
   }
 }
 
-template <int BLOCK>
 struct WaveState {
-  f32x16 o[QT][4];   // O^T tiles [q tile][d tile]: d = 32*dt + C row
-  float m[QT];       // running max (log2 domain), shared by lanes l, l^32
-  f32x4 l[QT];       // row sums (MFMA 16x16 C tile: lane c < 16 holds rows c, c + 16)
+  f32x16 o[4];   // O^T tiles [d tile]: d = 32*dt + C row
+  float m;       // running max (log2 domain), shared by lanes l, l^32
+  f32x4 l;       // row sums (MFMA 16x16 C tile: lane c < 16 holds rows c, c + 16)
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
@@ -308,15 +285,13 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid
   if (valid < BLOCK) {
     const int lim = valid - 4 * hl;   // key 4*hl + c is valid iff c < lim
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+    for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
-      for (int kt = 0; kt < TL::KTW; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
-          const int c = 32 * kt + 8 * (r / 4) + (r % 4);
-          sc.s[qt][kt][r] = c < lim ? sc.s[qt][kt][r] : -__builtin_inff();
-        }
+      for (int r = 0; r < 16; ++r) {
+        if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+        const int c = 32 * kt + 8 * (r / 4) + (r % 4);
+        sc.s[kt][r] = c < lim ? sc.s[kt][r] : -__builtin_inff();
+      }
   }
 }
 
@@ -339,33 +314,30 @@ __device__ __forceinline__ void mask_tail(Scores<BLOCK>& sc, int lane, int valid
 // recomputed here rather than held in a register through the loop.
 template <int BLOCK>
 __device__ __forceinline__ void mask_exact(Scores<BLOCK>& sc, uint32_t pat, int kfirst,
-                                           int valid, const int (&sec_from)[QT]) {
+                                           int valid, int sec_from) {
   using TL = Tile<BLOCK>;
   if (pat != 0xFu || valid < BLOCK) {
     const int lane = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
     const int hl = lane / 32, li = lane % 32;
+    const uint32_t bits = li >= sec_from ? pat >> 2 : pat;
+    const int klo = (bits & 1u) ? 0 : kfirst;
+    const int khi = (bits & 2u) ? valid : min(kfirst, valid);
+    const uint32_t shift = (uint32_t)(4 * hl - klo);
+    const uint32_t width = (uint32_t)max(khi - klo, 0);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      const uint32_t bits = li >= sec_from[qt] ? pat >> 2 : pat;
-      const int klo = (bits & 1u) ? 0 : kfirst;
-      const int khi = (bits & 2u) ? valid : min(kfirst, valid);
-      const uint32_t shift = (uint32_t)(4 * hl - klo);
-      const uint32_t width = (uint32_t)max(khi - klo, 0);
+    for (int kt = 0; kt < TL::KTW; ++kt)
 #pragma unroll
-      for (int kt = 0; kt < TL::KTW; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
-          const uint32_t c = (uint32_t)(32 * kt + 8 * (r / 4) + (r % 4));
-          sc.s[qt][kt][r] = c + shift < width ? sc.s[qt][kt][r] : -__builtin_inff();
-        }
-    }
+      for (int r = 0; r < 16; ++r) {
+        if (r % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+        const uint32_t c = (uint32_t)(32 * kt + 8 * (r / 4) + (r % 4));
+        sc.s[kt][r] = c + shift < width ? sc.s[kt][r] : -__builtin_inff();
+      }
   }
 }
 
 template <int BLOCK>
 struct Probs {
-  bf16x8 p[QT][Tile<BLOCK>::KTW][2];   // [q tile][key tile][k-step half]
+  bf16x8 p[Tile<BLOCK>::KTW][2];   // [key tile][k-step half]
 };
 
 // Softmax phase of the ping-pong schedule: block j's scores (in `sc`) become
@@ -376,44 +348,41 @@ struct Probs {
 // compiler from hoisting many exponentials at once (S, P, O and Q already
 // fill the register file).
 template <int BLOCK>
-__device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState<BLOCK>& st,
+__device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState& st,
                                               Probs<BLOCK>& pr, float scale_log2,
                                               const StepLoads<BLOCK>* sl) {
   using TL = Tile<BLOCK>;
-  constexpr int NE = 16 * TL::KTW;   // scores per lane per q tile
+  constexpr int NE = 16 * TL::KTW;   // scores per lane
   constexpr int NLOADS = 2 * TL::LOADS;
   constexpr int LOAD_EVERY = NE / NLOADS >= 2 ? NE / NLOADS : 2;   // scores per load
   int issued = 0;
+  float mx = -__builtin_inff();
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    float mx = -__builtin_inff();
+  for (int e = 0; e < NE; ++e) mx = fmaxf(mx, sc.s[e / 16][e % 16]);
+  const float m = pair_max(mx) * scale_log2;
+  const bool raise = m > st.m + RESCALE_SLACK;
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float a = raise ? __builtin_amdgcn_exp2f(st.m - m) : 1.f;
+    st.m = raise ? m : st.m;
+    // l tile: register 0 of lane c holds row c, register 1 row c + 16.
+    const float a16 = __shfl_xor(a, 16);
+    st.l[0] *= a;
+    st.l[1] *= a16;
 #pragma unroll
-    for (int e = 0; e < NE; ++e) mx = fmaxf(mx, sc.s[t][e / 16][e % 16]);
-    const float m = pair_max(mx) * scale_log2;
-    const bool raise = m > st.m[t] + RESCALE_SLACK;
-    if (__builtin_amdgcn_ballot_w64(raise)) {
-      const float a = raise ? __builtin_amdgcn_exp2f(st.m[t] - m) : 1.f;
-      st.m[t] = raise ? m : st.m[t];
-      // l tile: register 0 of lane c holds row c, register 1 row c + 16.
-      const float a16 = __shfl_xor(a, 16);
-      st.l[t][0] *= a;
-      st.l[t][1] *= a16;
+    for (int dt = 0; dt < 4; ++dt) st.o[dt] *= a;
+  }
+  const float msub = st.m == -__builtin_inff() ? 0.f : st.m;
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) st.o[t][dt] *= a;
-    }
-    const float msub = st.m[t] == -__builtin_inff() ? 0.f : st.m[t];
-#pragma unroll
-    for (int el = 0; el < NE; el += 2) {
-      if (el % 8 == 0) __builtin_amdgcn_sched_barrier(0);
-      if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
-      const float a = __builtin_amdgcn_exp2f(
-          __builtin_fmaf(sc.s[t][el / 16][el % 16], scale_log2, -msub));
-      const float b = __builtin_amdgcn_exp2f(
-          __builtin_fmaf(sc.s[t][(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
-      const bf16x2 pk = {(__bf16)a, (__bf16)b};
-      pr.p[t][el / 16][(el % 16) / 8][el % 8] = pk[0];
-      pr.p[t][el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
-    }
+  for (int el = 0; el < NE; el += 2) {
+    if (el % 8 == 0) __builtin_amdgcn_sched_barrier(0);
+    if (sl && el % LOAD_EVERY == 0 && issued < NLOADS) issue_step_load<BLOCK>(*sl, issued++);
+    const float a =
+        __builtin_amdgcn_exp2f(__builtin_fmaf(sc.s[el / 16][el % 16], scale_log2, -msub));
+    const float b = __builtin_amdgcn_exp2f(
+        __builtin_fmaf(sc.s[(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
+    const bf16x2 pk = {(__bf16)a, (__bf16)b};
+    pr.p[el / 16][(el % 16) / 8][el % 8] = pk[0];
+    pr.p[el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
   }
   if (sl)
     for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
@@ -425,12 +394,12 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
 // early and the tile loads in `sl` (may be null) spread over the phase.
 template <int BLOCK>
 __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
-                                           const bf16x8 (&qf)[QT][8], Scores<BLOCK>& sc,
-                                           const Probs<BLOCK>& pr, WaveState<BLOCK>& st,
+                                           const bf16x8 (&qf)[8], Scores<BLOCK>& sc,
+                                           const Probs<BLOCK>& pr, WaveState& st,
                                            const FragAddr& fa, const bf16x8& ones,
                                            const StepLoads<BLOCK>* sl) {
   using TL = Tile<BLOCK>;
-  constexpr int NS = 8 * TL::KTW;   // S MFMAs (per q tile): (key tile, d-step)
+  constexpr int NS = 8 * TL::KTW;   // S MFMAs: (key tile, d-step)
   constexpr int NP = 8 * TL::KTW;   // PV fragments: (d tile, key tile, k-step half)
   constexpr int NF = NS + NP;
   constexpr int AHEAD = 3;
@@ -463,35 +432,63 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
     if (sl && i % (NF / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NF / NLOADS));
     if (i < NP) {
       const int dt = i / (2 * TL::KTW), kt = (i / 2) % TL::KTW, c = i % 2;
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-        st.o[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], pr.p[qt][kt][c],
-                                                               st.o[qt][dt], 0, 0, 0);
+      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], pr.p[kt][c], st.o[dt], 0, 0, 0);
       if (i == NP - 1)
 #pragma unroll
         for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
 #pragma unroll
           for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt)
-              st.l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[qt][kt2][c2],
-                                                                 st.l[qt], 0, 0, 0);
+            st.l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[kt2][c2], st.l, 0, 0, 0);
     } else {
       const int f = i - NP;
       const int kt = f / 8, stp = f % 8;
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-        sc.s[qt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            fr[i], qf[qt][stp], stp == 0 ? f32x16{} : sc.s[qt][kt], 0, 0, 0);
+      sc.s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], qf[stp],
+                                                         stp == 0 ? f32x16{} : sc.s[kt], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// MODE: ATTN_DENSE (every key block), ATTN_BLOCK (block schedule words),
-// ATTN_EXACT (token-exact schedule words).  `sched_ptr` / `sched` are the
-// pair schedule (lvsa.h): row p lists the key blocks of query blocks 2p and
-// 2p+1.
+// Walk over CSR rows 2p ("row 0") and 2p+1 ("row 1") of a mask, from their
+// last entries down (see "The merged walk" above).  Row 1 starts where row 0
+// ends, so row 0's first entry is also the first entry of the pair.
+struct PairWalk {
+  int32_t i0, i1;     // next entry of row 0 / row 1 (walking down)
+  int32_t lo0, lo1;   // first entry of row 0 / row 1; a row is done below it
+  int32_t n;          // step words produced so far
+};
+
+// Step word of the next key block of the walk, from the candidates a (row
+// 0's entry i0) and b (row 1's entry i1); `prev` again when both rows are
+// done.  Block form (row entries are key blocks): kb in bits 0..29, bit 30 /
+// 31 set when row 0 / row 1 keeps it.  Token-exact form (row entries are
+// entry words): bits 0..23 kb and kfirst, bits 24..27 / 28..31 the patterns
+// of row 0 / row 1, 0 where that row does not keep kb.  A key block outside
+// [0, nb) costs a step that masks every key.
+template <int MODE>
+__device__ __forceinline__ uint32_t walk_next(PairWalk& pw, uint32_t a, uint32_t b,
+                                              uint32_t prev, int32_t nb) {
+  constexpr bool EXACT = MODE == ATTN_EXACT;
+  const int32_t ka = pw.i0 >= pw.lo0 ? (EXACT ? (int32_t)(a & 0xFFFFu) : (int32_t)a) : -1;
+  const int32_t kc = pw.i1 >= pw.lo1 ? (EXACT ? (int32_t)(b & 0xFFFFu) : (int32_t)b) : -1;
+  const int32_t kb = ka > kc ? ka : kc;
+  if (kb < 0) return prev;
+  const bool in0 = ka == kb, in1 = kc == kb;
+  pw.i0 -= in0 ? 1 : 0;
+  pw.i1 -= in1 ? 1 : 0;
+  pw.n += 1;
+  if (kb >= nb) return EXACT ? 0xFFFFu : 0x3FFFFFFFu;
+  if constexpr (EXACT) {
+    const uint32_t base = (in0 ? a : b) & 0xFFFFFFu;
+    return base | (in0 ? a & 0x0F000000u : 0u) | (in1 ? (b & 0x0F000000u) << 4 : 0u);
+  }
+  return (uint32_t)kb | (in0 ? 1u << 30 : 0u) | (in1 ? 1u << 31 : 0u);
+}
+
+typedef const __attribute__((address_space(1))) uint32_t global_u32;
+
+// MODE: ATTN_DENSE (every key block), ATTN_BLOCK (CSR rows of key blocks),
+// ATTN_EXACT (CSR rows of token-exact entry words).
 // One tile: head `tile / npairs`, pair of query blocks from `tile % npairs`,
 // using the workgroup's LDS stages `lds` (K slots 0-1, V slots 0-1).
 template <int BLOCK, int MODE>
@@ -500,7 +497,7 @@ __device__ __forceinline__ void attn_tile(
     const __bf16* __restrict__ vg, __bf16* __restrict__ og, int64_t q_sh,
     int64_t q_st, int64_t k_sh, int64_t k_st, int64_t v_sh, int64_t v_st,
     int64_t o_sh, int64_t o_st, int32_t H, int32_t N, int32_t nb,
-    const int32_t* __restrict__ sched_ptr, const uint32_t* __restrict__ sched,
+    const int32_t* __restrict__ row_ptr, const uint32_t* __restrict__ rows,
     int32_t P, float scale_log2) {
   using TL = Tile<BLOCK>;
   constexpr bool SPARSE = MODE != ATTN_DENSE;
@@ -523,7 +520,7 @@ __device__ __forceinline__ void attn_tile(
   const int pq = npairs - 1 - tile % npairs;    // query blocks 2pq, 2pq+1
   const bool upper = wave >= TL::NW / 2;        // rows of query block 2pq+1
   const int qb = 2 * pq + (upper ? 1 : 0);
-  const int rows0 = 32 * QT * (wave % (TL::NW / 2));   // first row within qb
+  const int rows0 = 32 * (wave % (TL::NW / 2));   // first row within qb
 
   const __bf16* qh = qg + head * q_sh;
   __bf16* oh = og + head * o_sh;
@@ -533,8 +530,7 @@ __device__ __forceinline__ void attn_tile(
   const uint32_t v_bytes = (uint32_t)(((int64_t)(N - 1) * v_st + D) * 2);
   const LoadPlan<BLOCK> kp = load_plan<BLOCK>((uint32_t)(k_st * 2), wave, lane);
   const LoadPlan<BLOCK> vp = load_plan<BLOCK>((uint32_t)(v_st * 2), wave, lane);
-  // Schedule words: key block in bits 0..29 (block form) or 0..15 (exact
-  // form); the words of a row are walked last to first (below).
+  // Step words: key block in bits 0..29 (block form) or 0..15 (exact form).
   auto kb_of = [&](uint32_t w) {
     return (int)(EXACT ? (w & 0xFFFFu) : (w & 0x3FFFFFFFu));
   };
@@ -546,33 +542,24 @@ __device__ __forceinline__ void attn_tile(
   };
   const FragAddr fa = frag_addr(lane);
 
-  // Q fragments: rows qrow0 + 32*qt, k-slots d = 16*stp + 8*hl + 0..7.
-  const int qrow0 = qb * BLOCK + rows0 + li;
-  bf16x8 qf[QT][8];
+  // Q fragments: row qrow, k-slots d = 16*stp + 8*hl + 0..7.
+  const int qrow = qb * BLOCK + rows0 + li;
+  bf16x8 qf[8];
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const int qrow = qrow0 + 32 * qt;
-#pragma unroll
-    for (int stp = 0; stp < 8; ++stp)
-      qf[qt][stp] = qrow < N
-                        ? *(const bf16x8*)(qh + (int64_t)qrow * q_st + 16 * stp + 8 * hl)
-                        : bf16x8{};
-  }
+  for (int stp = 0; stp < 8; ++stp)
+    qf[stp] = qrow < N ? *(const bf16x8*)(qh + (int64_t)qrow * q_st + 16 * stp + 8 * hl)
+                       : bf16x8{};
 
-  // Exact mode: the first of the wave's 32 rows (per q tile) that lies in
-  // the query block's second frame (the first frame holds the block's first
-  // qfirst rows; P >= BLOCK, so there are at most two); wave-uniform.
-  int sec_from[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) sec_from[qt] = 32;
+  // Exact mode: the first of the wave's 32 rows that lies in the query
+  // block's second frame (the first frame holds the block's first qfirst
+  // rows; P >= BLOCK, so there are at most two); wave-uniform.
+  int sec_from = 32;
   if constexpr (EXACT) {
     const int qfirst = P - (int)(((int64_t)qb * BLOCK) % P);
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
-      sec_from[qt] = __builtin_amdgcn_readfirstlane(qfirst - rows0 - 32 * qt);
+    sec_from = __builtin_amdgcn_readfirstlane(qfirst - rows0);
   }
-  // Masks the scores of the key block of schedule word w for this wave's
-  // query block: a key block that block does not keep has no valid keys.
+  // Masks the scores of the key block of step word w for this wave's query
+  // block: a key block that block does not keep has no valid keys.
   const uint32_t kept_bit = upper ? 31u : 30u;       // block form
   const uint32_t pat_shift = upper ? 28u : 24u;      // exact form
   auto mask_block = [&](Scores<BLOCK>& sc, uint32_t w) {
@@ -584,41 +571,62 @@ __device__ __forceinline__ void attn_tile(
       mask_tail<BLOCK>(sc, lane, ((w >> kept_bit) & 1u) ? N - kb * BLOCK : 0);
   };
 
-  int beg = 0, n = nb;
+  // The walk (sparse modes) or the key blocks nb-1 .. 0 (dense).  Words of
+  // steps past the last one repeat it: their loads land in slots that no
+  // later step reads.  Every row entry the walk loads is an entry of the
+  // pair (an exhausted row's lane reads the pair's first entry instead), so
+  // no load leaves the mask's arrays.
+  PairWalk pw{};
+  uint32_t w0 = 0u, w1 = 0u, w2 = 0u;
+  global_u32* const rg = (global_u32*)rows;
   if constexpr (SPARSE) {
-    // Uniform by construction; the pair offsets share their array with the
-    // kernel's tile counters, so the compiler loads them per lane.
-    beg = __builtin_amdgcn_readfirstlane(sched_ptr[pq]);
-    n = __builtin_amdgcn_readfirstlane(sched_ptr[pq + 1]) - beg;
+    const int32_t r0 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq]);
+    const int32_t r1 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 1]);
+    const int32_t r2 =
+        2 * pq + 1 < nb ? __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 2]) : r1;
+    pw.lo0 = r0;
+    pw.i0 = r1 - 1;
+    pw.lo1 = r1;
+    pw.i1 = r2 - 1;
+    if (r0 < r2) {
+      // The first three merges read at most the last three entries of each
+      // row: one load, lanes 0..2 row 0 from its end, lanes 3..5 row 1.
+      const int32_t want = lane < 3 ? pw.i0 - lane : pw.i1 - (lane - 3);
+      const int32_t from = lane < 3 ? pw.lo0 : pw.lo1;
+      const uint32_t first = rg[want >= from ? want : r0];
+      auto cand = [&](int row) {
+        const int32_t used = row == 0 ? r1 - 1 - pw.i0 : r2 - 1 - pw.i1;
+        return (uint32_t)__builtin_amdgcn_readlane((int)first, 3 * row + min(used, 2));
+      };
+      w0 = walk_next<MODE>(pw, cand(0), cand(1), 0u, nb);
+      w1 = walk_next<MODE>(pw, cand(0), cand(1), w0, nb);
+      w2 = walk_next<MODE>(pw, cand(0), cand(1), w1, nb);
+    }
+  } else {
+    pw.n = nb;
+    w0 = (uint32_t)(nb - 1) | 0xC0000000u;
+    w1 = (uint32_t)max(nb - 2, 0) | 0xC0000000u;
+    w2 = (uint32_t)max(nb - 3, 0) | 0xC0000000u;
   }
-  // Step j takes the row's word n-1-j: key blocks in descending order.  With
-  // the pairs of a head dispatched last to first, a workgroup started later
-  // holds keys further left, so it reaches the blocks it shares with the
-  // workgroups started before it after fewer steps of its own, while they are
-  // still in L2 (the same holds for ascending walks of ascending pairs); the
-  // key blocks every row keeps (text tokens, at the end) come first.
-  auto word_at = [&](int j) -> uint32_t {   // schedule word of step j
-    return SPARSE ? sched[beg + n - 1 - j] : ((uint32_t)(n - 1 - j) | 0xC0000000u);
-  };
-  // The word of step j+3 is fetched by a vector load one step before it is
-  // needed, so the load's latency hides under a whole step (a scalar load
-  // would be waited for at the next LDS wait, which shares its counter).
-  const __amdgpu_buffer_rsrc_t rsched = make_rsrc(
-      sched, SPARSE ? (uint32_t)__builtin_amdgcn_readfirstlane(sched_ptr[npairs] * 4) : 0u);
-  auto word_fetch = [&](int j) -> uint32_t {   // VGPR value, clamped to the row
-    const int jj = j < n ? n - 1 - j : 0;
-    if constexpr (!SPARSE) return (uint32_t)jj | 0xC0000000u;
-    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsched, (beg + jj) * 4, 0, 0);
+  // Candidates of the merge at the end of a step: lane 0 row 0's entry i0,
+  // lane 1 row 1's entry i1.  A vector load, so that its wait is the step's
+  // final vmcnt(0) rather than the next LDS wait, whose counter a scalar load
+  // would share.
+  auto fetch_candidates = [&]() -> uint32_t {
+    if constexpr (SPARSE) {
+      const int32_t i0 = pw.i0 >= pw.lo0 ? pw.i0 : pw.lo0;
+      const int32_t i1 = pw.i1 >= pw.lo1 ? pw.i1 : pw.lo0;
+      return rg[lane == 0 ? i0 : i1];
+    } else {
+      return 0u;
+    }
   };
 
-  WaveState<BLOCK> ws;
+  WaveState ws;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) ws.o[qt][dt] = f32x16{};
-    ws.m[qt] = -__builtin_inff();
-    ws.l[qt] = f32x4{};
-  }
+  for (int dt = 0; dt < 4; ++dt) ws.o[dt] = f32x16{};
+  ws.m = -__builtin_inff();
+  ws.l = f32x4{};
   // A operand of the row-sum MFMA (16x16x32): read as P^T's B operand, lane
   // group g = lane/16 of the 32x32 P register holds q rows 16*(g%2) + 0..15,
   // so A row 0 takes groups 0 and 2 (rows 0-15) and row 1 groups 1 and 3.
@@ -630,7 +638,7 @@ __device__ __forceinline__ void attn_tile(
     for (int e = 0; e < 8; ++e) ones[e] = one ? (__bf16)1.f : (__bf16)0.f;
   }
 
-  if (n > 0) {
+  if (pw.n > 0) {
     // LDS stages: K(b) in K slot b % 2, V(b) in V slot b % 2.
     const uint32_t k_slot0 = lds_base, v_slot0 = lds_base + 2 * TL::BYTES;
     const char* const k_lds = lds;
@@ -646,9 +654,6 @@ __device__ __forceinline__ void attn_tile(
     // in half-period 2j (into the slots of K(j) and V(j-1), free since
     // half-period 2j-1) and waited for at the end of 2j+1.
     const bool lead = !upper;
-    const uint32_t w0 = word_at(0);
-    uint32_t w1 = n > 1 ? word_at(1) : w0;     // step j+1
-    uint32_t w2 = n > 2 ? word_at(2) : w1;     // step j+2
     issue_tile<BLOCK>(k_slot0, rk_at(w0), kp);
     issue_tile<BLOCK>(v_slot0, rv_at(w0), vp);
     issue_tile<BLOCK>(k_slot0 + TL::BYTES, rk_at(w1), kp);
@@ -659,8 +664,8 @@ __device__ __forceinline__ void attn_tile(
     Probs<BLOCK> pr;
     if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
     __syncthreads();
-    for (int j = 0; j < n; ++j) {
-      const uint32_t w3v = word_fetch(j + 3);
+    for (int j = 0; j < pw.n; ++j) {
+      const uint32_t cv = fetch_candidates();
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
@@ -677,48 +682,47 @@ __device__ __forceinline__ void attn_tile(
       __syncthreads();
       // half-period 2j+1
       if (lead) {
-        if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
+        if (j + 1 < pw.n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
       } else {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
         mask_block(sc, w1);
       }
       wait_loads_and_sync();
+      uint32_t w3;
+      if constexpr (SPARSE) {
+        w3 = walk_next<MODE>(pw, (uint32_t)__builtin_amdgcn_readlane((int)cv, 0),
+                             (uint32_t)__builtin_amdgcn_readlane((int)cv, 1), w2, nb);
+      } else {
+        w3 = (uint32_t)max(nb - 4 - j, 0) | 0xC0000000u;
+      }
       w1 = w2;
-      w2 = __builtin_amdgcn_readfirstlane(w3v);
+      w2 = w3;
     }
     __syncthreads();
   }
 
   // Every wave holds whole rows: O / l, rounded to bf16.  The l tile holds
   // row c in register 0 of lane c and row c + 16 in register 1 (c < 16).
-  float lsum[QT];
+  const float r0s = __shfl(ws.l[0], li), r1s = __shfl(ws.l[1], li & 15);
+  const float lsum = li < 16 ? r0s : r1s;
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  if (qrow < N) {
+    __bf16* orow = oh + (int64_t)qrow * o_st;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const float r0 = __shfl(ws.l[qt][0], li), r1 = __shfl(ws.l[qt][1], li & 15);
-    lsum[qt] = li < 16 ? r0 : r1;
-  }
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const float inv = lsum[qt] > 0.f ? 1.f / lsum[qt] : 0.f;
-    const int qrow = qrow0 + 32 * qt;
-    if (qrow < N) {
-      __bf16* orow = oh + (int64_t)qrow * o_st;
+      for (int a = 0; a < 4; ++a) {
+        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+        bf16x4 w;
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-          bf16x4 w;
-#pragma unroll
-          for (int b = 0; b < 4; ++b) w[b] = (__bf16)(ws.o[qt][dt][4 * a + b] * inv);
-          *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
-        }
-    }
+        for (int b = 0; b < 4; ++b) w[b] = (__bf16)(ws.o[dt][4 * a + b] * inv);
+        *(bf16x4*)(orow + 32 * dt + 8 * a + 4 * hl) = w;
+      }
   }
 }
 
-// First tile and tile count of XCD x's share of `total` tiles (contiguous,
-// as xcd_remap deals them).
+// First tile and tile count of XCD x's share of `total` tiles: contiguous
+// shares, the first total % 8 of them one tile larger.
 __device__ __forceinline__ int xcd_first(int x, int total) {
   const int per = total / 8, rem = total % 8;
   return x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
@@ -727,19 +731,30 @@ __device__ __forceinline__ int xcd_count(int x, int total) {
   return total / 8 + (x < total % 8 ? 1 : 0);
 }
 
-// Next tile for a workgroup on XCD `xcd`: the next one of its own XCD's share
-// (ctr[x] counts the tiles handed out of XCD x's share), else the next one of
-// another XCD's share, so XCDs that run faster take on more tiles; -1 when
-// every share is handed out.  Every call advances at most 8 counters by one,
-// so a workgroup's loop ends after at most total + 8 calls.
-__device__ __forceinline__ int fetch_tile(uint32_t* ctr, int xcd, int total) {
+// Next tile for a workgroup on XCD `xcd`, or -1 when every tile is handed
+// out.  Tiles are dealt to the XCDs in contiguous shares; a workgroup takes
+// the next tile from the front of its own XCD's share and, once that share
+// is handed out, the last one left at the back of another XCD's share, so
+// XCDs that clock faster take on more tiles while each share is still
+// worked from its front by its own XCD (neighbouring tiles, whose key lists
+// overlap, stay together in that XCD's L2).  Counter word x holds in bits
+// 0..31 the takes from the front of share x and in bits 32..63 those from
+// its back; a take gets a tile iff the two counts before it sum to less
+// than the share's size, so each tile goes out once.  Every call makes at
+// most 8 atomic adds, so a workgroup's loop ends after at most total + 8
+// calls.
+__device__ __forceinline__ int fetch_tile(uint64_t* ctr, int xcd, int total) {
   for (int d = 0; d < 8; ++d) {
     const int x = (xcd + d) % 8;
-    const uint32_t cnt = (uint32_t)xcd_count(x, total);
-    if (__hip_atomic_load(&ctr[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= cnt)
-      continue;
-    const uint32_t c = atomicAdd(&ctr[x], 1u);
-    if (c < cnt) return xcd_first(x, total) + (int)c;
+    const uint64_t cnt = (uint64_t)xcd_count(x, total);
+    const uint64_t seen =
+        __hip_atomic_load(&ctr[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((seen & 0xFFFFFFFFull) + (seen >> 32) >= cnt) continue;
+    const uint64_t old = __hip_atomic_fetch_add(&ctr[x], d == 0 ? 1ull : 1ull << 32,
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t front = old & 0xFFFFFFFFull, back = old >> 32;
+    if (front + back < cnt)
+      return xcd_first(x, total) + (d == 0 ? (int)front : (int)(cnt - 1 - back));
   }
   return -1;
 }
@@ -752,8 +767,9 @@ struct KArgs {
   const __bf16* v;
   __bf16* o;
   int64_t q_sh, q_st, k_sh, k_st, v_sh, v_st, o_sh, o_st;
-  const int32_t* sched_ptr;
-  const uint32_t* sched;
+  const int32_t* row_ptr;
+  const uint32_t* rows;
+  uint64_t* counters;
   int32_t H, N, nb, P;
   float scale_log2;
 };
@@ -761,51 +777,39 @@ struct KArgs {
 template <int BLOCK, int MODE>
 __device__ __forceinline__ void attn_tile_args(char* lds, int tile, const KArgs& a) {
   attn_tile<BLOCK, MODE>(lds, tile, a.q, a.k, a.v, a.o, a.q_sh, a.q_st, a.k_sh, a.k_st,
-                         a.v_sh, a.v_st, a.o_sh, a.o_st, a.H, a.N, a.nb, a.sched_ptr,
-                         a.sched, a.P, a.scale_log2);
+                         a.v_sh, a.v_st, a.o_sh, a.o_st, a.H, a.N, a.nb, a.row_ptr,
+                         a.rows, a.P, a.scale_log2);
 }
 
-// Block-sparse and token-exact attention: persistent workgroups, one per CU,
-// take tiles until all are done; ctr (16 words after the pair schedule's
-// offsets, zero on entry) holds the 8 per-XCD tile counters and the count of
-// finished workgroups, and the last workgroup to finish sets them back to
-// zero.  Dense attention: one workgroup per tile, dealt to XCDs by
-// xcd_remap.  `sched_ptr` / `sched` are the pair schedule (lvsa.h).
+// Persistent workgroups, at most one per CU, take tiles until all are done
+// (fetch_tile), through the launch's own counters, zeroed by
+// zero_counters_kernel just before on the same stream.
 template <int BLOCK, int MODE>
 __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(const KArgs args) {
   __shared__ __attribute__((aligned(1024))) char lds[4 * Tile<BLOCK>::BYTES];
-  const int npairs = (args.nb + 1) / 2;
-  const int total = npairs * args.H;
-  if constexpr (MODE == ATTN_DENSE) {
-    attn_tile_args<BLOCK, MODE>(lds, xcd_remap(blockIdx.x, total), args);
-  } else {
-    __shared__ int next_tile;
-    uint32_t* const ctr = (uint32_t*)(const_cast<int32_t*>(args.sched_ptr) + npairs + 1);
-    // Workgroups are dispatched round-robin over the 8 XCDs.
-    const int xcd = blockIdx.x % 8;
-    for (;;) {
-      if (threadIdx.x == 0) next_tile = fetch_tile(ctr, xcd, total);
-      __syncthreads();
-      const int tile = __builtin_amdgcn_readfirstlane(next_tile);
-      __syncthreads();   // every wave has read next_tile before it is rewritten
-      if (tile < 0) break;
-      // The arguments are the first kernel argument; an offset the compiler
-      // cannot see to be zero makes every tile load them afresh (scalar
-      // loads), so they are not live across tiles.
-      int zero = 0;
-      asm volatile("" : "+v"(zero));
-      zero = __builtin_amdgcn_readfirstlane(zero);
-      const KArgs* ap = (const KArgs*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() + zero);
-      attn_tile_args<BLOCK, MODE>(lds, tile, *ap);
-    }
-    if (threadIdx.x == 0) {
-      __threadfence();
-      if (atomicAdd(&ctr[8], 1u) == gridDim.x - 1) {
-        __threadfence();
-        for (int x = 0; x < 9; ++x) atomicExch(&ctr[x], 0u);
-      }
-    }
+  __shared__ int next_tile;
+  const int total = (args.nb + 1) / 2 * args.H;
+  // Workgroups are dispatched round-robin over the 8 XCDs.
+  const int xcd = blockIdx.x % 8;
+  for (;;) {
+    if (threadIdx.x == 0) next_tile = fetch_tile(args.counters, xcd, total);
+    __syncthreads();
+    const int tile = __builtin_amdgcn_readfirstlane(next_tile);
+    __syncthreads();   // every wave has read next_tile before it is rewritten
+    if (tile < 0) break;
+    // The arguments are the first kernel argument; an offset the compiler
+    // cannot see to be zero makes every tile load them afresh (scalar
+    // loads), so they are not live across tiles.
+    int zero = 0;
+    asm volatile("" : "+v"(zero));
+    zero = __builtin_amdgcn_readfirstlane(zero);
+    const KArgs* ap = (const KArgs*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() + zero);
+    attn_tile_args<BLOCK, MODE>(lds, tile, *ap);
   }
+}
+
+__global__ __launch_bounds__(64) void zero_counters_kernel(uint64_t* __restrict__ ctr) {
+  if (threadIdx.x < kTileCounters) ctr[threadIdx.x] = 0;
 }
 
 // Compute units of the current device (cached per device).
@@ -827,9 +831,9 @@ template <int BLOCK, int MODE>
 hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)D);
   const int tiles = (a.n_blocks + 1) / 2 * a.heads;
-  // Block-sparse and token-exact: one persistent workgroup per CU (each
-  // takes 128 KB of LDS, so one fits a CU); dense: one workgroup per tile.
-  const int grid = MODE == ATTN_DENSE ? tiles : (tiles < cu_count() ? tiles : cu_count());
+  // One persistent workgroup per CU (each takes 128 KB of LDS, so one fits
+  // a CU), or one per tile when there are fewer tiles.
+  const int grid = tiles < cu_count() ? tiles : cu_count();
   KArgs k;
   k.q = (const __bf16*)a.q;
   k.k = (const __bf16*)a.k;
@@ -837,10 +841,12 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   k.o = (__bf16*)a.o;
   k.q_sh = a.q_sh; k.q_st = a.q_st; k.k_sh = a.k_sh; k.k_st = a.k_st;
   k.v_sh = a.v_sh; k.v_st = a.v_st; k.o_sh = a.o_sh; k.o_st = a.o_st;
-  k.sched_ptr = a.pair_ptr;
-  k.sched = a.pair_word;
+  k.row_ptr = a.row_ptr;
+  k.rows = a.rows;
+  k.counters = a.counters;
   k.H = a.heads; k.N = a.n_tokens; k.nb = a.n_blocks; k.P = a.frame_tokens;
   k.scale_log2 = scale_log2;
+  hipLaunchKernelGGL(zero_counters_kernel, dim3(1), dim3(64), 0, stream, a.counters);
   hipLaunchKernelGGL((attn_fwd_kernel<BLOCK, MODE>), dim3(grid), dim3(Tile<BLOCK>::NT), 0,
                      stream, k);
   return hipGetLastError();

@@ -20,7 +20,7 @@ struct FrameCfg {
   int32_t extra;     // dedicated initial anchors: frames 0..extra-1
   int32_t g;         // |G|: Eq. 3 (or Def. 2) anchors plus the extra ones
   int32_t text;      // text tokens after the T*P video tokens (segment T)
-  int32_t s0;        // s mod T_per (0 for fixed anchors)
+  int32_t s0;        // (s mod T_per) mod T (0 for fixed anchors)
   int32_t mode;      // LVSA_WINDOW_*
   int32_t rotate;    // Eq. 3 (1) or Def. 2's fixed set (0)
   int32_t tie_high;  // Alg. 1 equal-room rule
@@ -34,9 +34,10 @@ __host__ __device__ inline int32_t imax(int32_t a, int32_t b) { return a > b ? a
 
 // Membership of frame f in the anchor set.
 //   rotate = 0: Def. 2, f mod T_per == 0.
-//   rotate = 1: Eq. 3, f = (s0 + i*T_per) mod T for some 0 <= i < k.  The
-//   unreduced value s0 + i*T_per is below k*T_per <= T + T_per - 1 < 2T, so
-//   it equals either f or f + T.
+//   rotate = 1: Eq. 3, f = (s0 + i*T_per) mod T for some 0 <= i < k, with
+//   s0 = (s mod T_per) mod T < T.  When T_per <= T the unreduced value
+//   s0 + i*T_per stays below s0 + (k-1)*T_per <= T + T_per - 2 < 2T, so it
+//   equals either f or f + T; when T_per > T, k = 1 and the only anchor is s0.
 //   f < extra: a dedicated initial anchor.
 __host__ __device__ inline bool is_anchor(const FrameCfg& c, int32_t f) {
   if (f < c.extra) return true;
@@ -47,44 +48,90 @@ __host__ __device__ inline bool is_anchor(const FrameCfg& c, int32_t f) {
   return u % c.tper == 0 && u / c.tper < c.k;
 }
 
+// Anchors of the period rule alone (Eq. 3 or Def. 2) among frames 0..f-1,
+// 0 <= f <= T, in closed form.  Eq. 3's anchors are two ascending runs: the
+// values s0 + i*T_per that stay below T (the first n_a of them), then the
+// wrapped ones s0 + i*T_per - T (i = n_a..k-1), which all lie below s0.
+__host__ __device__ inline int32_t period_anchors_below(const FrameCfg& c, int32_t f) {
+  if (!c.rotate) return ceil_div(imin(f, c.T), c.tper);
+  const int32_t n_a = imin(c.k, ceil_div(c.T - c.s0, c.tper));
+  const int32_t run_a = f <= c.s0 ? 0 : imin(n_a, ceil_div(f - c.s0, c.tper));
+  const int32_t run_b = imax(0, imin(c.k, ceil_div(f + c.T - c.s0, c.tper)) - n_a);
+  return run_a + run_b;
+}
+
+// All anchors (the period rule's and frames 0..extra-1) among frames 0..f-1.
+__host__ __device__ inline int32_t anchors_below(const FrameCfg& c, int32_t f) {
+  const int32_t e = imin(imin(c.extra, c.T), f);
+  return period_anchors_below(c, f) + e - period_anchors_below(c, e);
+}
+
+// Frames of [lo, hi] that are not anchors.
+__host__ __device__ inline int32_t free_frames(const FrameCfg& c, int32_t lo, int32_t hi) {
+  return (hi - lo + 1) - (anchors_below(c, hi + 1) - anchors_below(c, lo));
+}
+
+// Expanded window (Alg. 1).  Alg. 1 widens the adaptive window [l, h] one
+// frame at a time on the side with more room (room below a = l, above
+// b = T-1-h; equal room goes to the low side, or to the high side under
+// tie_high) until the window holds min(2W+1, T-|G|) frames that are not
+// anchors, or spans every frame.  The room rule fixes the order in which
+// frames join: the roomier side alone until the two rooms are equal, then
+// the two sides in turn, the tie side first.  So the window after g growth
+// steps has a closed form, its count of non-anchor frames never decreases
+// with g, and Alg. 1's number of steps is the least g in [0, a + b] whose
+// window holds enough of them (a binary search over g).
+__host__ __device__ inline void grown_window(int32_t l, int32_t h, int32_t a, int32_t b,
+                                             int32_t g, bool tie_high, int32_t* lo,
+                                             int32_t* hi) {
+  const int32_t d = a > b ? a - b : b - a;   // steps before the rooms are equal
+  int32_t grow_lo, grow_hi;
+  if (g <= d) {
+    grow_lo = a > b ? g : 0;
+    grow_hi = a > b ? 0 : g;
+  } else {
+    const int32_t r = g - d;                  // steps taken in turn
+    const int32_t first = (r + 1) / 2, second = r / 2;
+    grow_lo = (a > b ? d : 0) + (tie_high ? second : first);
+    grow_hi = (b > a ? d : 0) + (tie_high ? first : second);
+  }
+  *lo = l - grow_lo;
+  *hi = h + grow_hi;
+}
+
 // Window [lo, hi] of query frame t under the configured rule.
 //   BASIC    Def. 2
 //   ADAPTIVE shifted to keep 2W+1 frames (Sec. 2, "Overlapping frames")
-//   EXPANDED Alg. 1: grow the adaptive window on the side with more room
-//            until min(2W+1, T-|G|) of its frames are not anchors.
+//   EXPANDED Alg. 1, as above
 // Returns the number of Alg. 1 growth steps (0 for the other rules).
 __host__ __device__ inline int32_t frame_window(const FrameCfg& c, int32_t t,
                                                 int32_t* lo_out,
                                                 int32_t* hi_out) {
   const int32_t T = c.T, W = c.W;
-  int32_t lo, hi;
   if (c.mode == LVSA_WINDOW_BASIC) {
-    lo = imax(0, t - W);
-    hi = imin(T - 1, t + W);
-    *lo_out = lo;
-    *hi_out = hi;
+    *lo_out = imax(0, t - W);
+    *hi_out = imin(T - 1, t + W);
     return 0;
   }
-  lo = imax(0, imin(t - W, T - 1 - 2 * W));
-  hi = imin(T - 1, imax(t + W, 2 * W));
+  const int32_t l = imax(0, imin(t - W, T - 1 - 2 * W));
+  const int32_t h = imin(T - 1, imax(t + W, 2 * W));
   int32_t steps = 0;
   if (c.mode == LVSA_WINDOW_EXPANDED) {
     const int32_t target = imin(2 * W + 1, T - c.g);
-    int32_t nonglobal = 0;
-    for (int32_t f = lo; f <= hi; ++f) nonglobal += is_anchor(c, f) ? 0 : 1;
-    while (nonglobal < target && (lo > 0 || hi < T - 1)) {
-      const int32_t room_lo = lo, room_hi = T - 1 - hi;
-      int32_t f;
-      if (room_lo > room_hi || (room_lo == room_hi && !c.tie_high))
-        f = --lo;
+    const int32_t a = l, b = T - 1 - h;
+    int32_t g_lo = 0, g_hi = a + b;
+    while (g_lo < g_hi) {
+      const int32_t g = (g_lo + g_hi) / 2;
+      int32_t lo, hi;
+      grown_window(l, h, a, b, g, c.tie_high != 0, &lo, &hi);
+      if (free_frames(c, lo, hi) >= target)
+        g_hi = g;
       else
-        f = ++hi;
-      nonglobal += is_anchor(c, f) ? 0 : 1;
-      ++steps;
+        g_lo = g + 1;
     }
+    steps = g_lo;
   }
-  *lo_out = lo;
-  *hi_out = hi;
+  grown_window(l, h, l, T - 1 - h, steps, c.tie_high != 0, lo_out, hi_out);
   return steps;
 }
 
@@ -148,20 +195,6 @@ __host__ __device__ inline uint32_t exact_entry(int32_t kb, int32_t f0,
   uint32_t kfirst;
   key_block_split(kb, T, P, B, N, &g0, &g1, &kfirst);
   return exact_word(kb, g0, g1, kfirst, f0, f1, attends);
-}
-
-// Pair schedule words (lvsa.h, "pair schedule"): key block kb listed for the
-// query-block pair (2p, 2p+1), with which of the two keeps it.
-__host__ __device__ inline uint32_t pair_word_of(int32_t kb, bool kept0, bool kept1) {
-  return (uint32_t)kb | (kept0 ? 1u << 30 : 0u) | (kept1 ? 1u << 31 : 0u);
-}
-
-// Token-exact pair word from the entry words e0 of (2p, kb) and e1 of
-// (2p+1, kb), each 0 when that query block does not keep kb (a kept block's
-// pattern is never 0): kb and kfirst, then the two 4-bit patterns.
-__host__ __device__ inline uint32_t pair_exact_word(uint32_t e0, uint32_t e1) {
-  const uint32_t base = (e0 != 0u ? e0 : e1) & 0xFFFFFFu;
-  return base | (((e0 >> 24) & 0xFu) << 24) | (((e1 >> 24) & 0xFu) << 28);
 }
 
 // Whether a block mask of (P, B, nb) can carry exact entry words.

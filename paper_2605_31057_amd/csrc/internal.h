@@ -32,30 +32,23 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<int32_t>* col_idx,
                     std::vector<uint32_t>* entry);
 
-// Pair schedule from a CSR (mask_host.cpp): row p lists the key blocks of
-// query blocks 2p and 2p+1 (lvsa.h, "pair schedule"); `pair_exact` (may be
-// null, and is ignored when `entry` is null) receives the token-exact words.
-void build_pairs_host(const std::vector<int32_t>& row_ptr,
-                      const std::vector<int32_t>& col_idx,
-                      const std::vector<uint32_t>* entry,
-                      std::vector<int32_t>* pair_ptr,
-                      std::vector<uint32_t>* pair_word,
-                      std::vector<uint32_t>* pair_exact);
-
 // Device mask construction (mask_device.hip).  Writes row_ptr and, where the
-// pointer is non-null, col_idx and/or the token-exact entry words, then the
-// pair schedule (pair_ptr and pair words, in the token-exact form when
-// `exact`).  The builder holds the windows of one query-block pair's frames
-// in LDS: device_mask_supported says whether a pair touches few enough frames.
+// pointer is non-null, col_idx and/or the token-exact entry words.  The
+// builder holds the windows of one query-block pair's frames in LDS:
+// device_mask_supported says whether a pair touches few enough frames.
 bool device_mask_supported(const FrameCfg& c, int32_t P, int32_t B);
 hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
-                                    uint32_t* d_entry, int32_t* d_pair_ptr,
-                                    uint32_t* d_pair_word, bool exact,
-                                    hipStream_t stream);
+                                    uint32_t* d_entry, hipStream_t stream);
+
+// Tile counters of one attention launch: eight 64-bit words (one per XCD),
+// zeroed on the launch stream before the kernel runs.
+constexpr int kTileCounters = 8;
 
 // Attention launch (attention.hip).  Pointers are bf16 tensors; strides in
-// elements.  pair_ptr/pair_word are null for the dense pass.
+// elements.  The sparse modes read the CSR rows of each pair of query blocks
+// (col_idx for ATTN_BLOCK, entry words for ATTN_EXACT); row_ptr and rows are
+// null for the dense pass.
 struct AttnArgs {
   const void* q;
   const void* k;
@@ -65,12 +58,26 @@ struct AttnArgs {
   int32_t heads;
   int32_t n_tokens;
   int32_t n_blocks;
-  const int32_t* pair_ptr;   // pair schedule rows [ceil(nb/2) + 1]
-  const uint32_t* pair_word; // block or token-exact (ATTN_EXACT) pair words
+  const int32_t* row_ptr;    // [n_blocks + 1]
+  const uint32_t* rows;      // col_idx (block form) or entry words (exact form)
   int32_t frame_tokens;      // P (ATTN_EXACT only)
+  uint64_t* counters;        // kTileCounters words, any content (zeroed here)
 };
 enum AttnMode { ATTN_DENSE = 0, ATTN_BLOCK = 1, ATTN_EXACT = 2 };
 hipError_t launch_attention(const AttnArgs& a, int32_t block, AttnMode mode,
                             hipStream_t stream);
+
+// Per-device pool of tile-counter sets (api.cpp).  acquire hands out a set no
+// launch in flight uses; release records, after the launch on `stream`, the
+// event that frees it again (or keeps the set for good when the stream is
+// being captured into a graph).
+struct CounterLease {
+  int device = -1;
+  int32_t slot = -1;
+  uint64_t* counters = nullptr;
+  bool captured = false;
+};
+lvsa_status acquire_counters(hipStream_t stream, CounterLease* lease);
+void release_counters(const CounterLease& lease, hipStream_t stream);
 
 }  // namespace lvsa

@@ -2,22 +2,19 @@
 //
 // Computes the same block CSR as the host builder (the LVSA frame sets of
 // Sec. 2: Def. 2, Eq. 3, Alg. 1, expanded to blocks by the any-overlap rule)
-// and the pair schedule the attention kernel reads, without a host round
-// trip, so a denoising loop can rebuild the mask for step s on the stream
-// that then runs attention.
+// without a host round trip, so a denoising loop can rebuild the mask for
+// step s on the stream that then runs attention.
 //
-// Four launches on the stream, each workgroup handling a pair of query
-// blocks 2p and 2p+1 (the last pair of an odd nb has one): the CSR rows of
-// both blocks and the pair row (a key block is listed when either keeps it)
-// come from the same tests:
+// Three launches on the stream, each workgroup of the first and the last
+// handling a pair of query blocks 2p and 2p+1 (the last pair of an odd nb has
+// one), whose frames overlap, so the windows are computed once for both:
 //   1. one workgroup per pair: the windows of the pair's frames (Alg. 1) into
 //      LDS, then every key block tested in parallel against both query
-//      blocks; the three row lengths go to row_ptr[qb + 1] and pair_ptr[p + 1];
-//   2, 3. one workgroup each: in-place inclusive scans of row_ptr and pair_ptr;
-//   4. one workgroup per pair: the same tests again, listed key blocks
+//      blocks; the two row lengths go to row_ptr[qb + 1];
+//   2. one workgroup: an in-place inclusive scan of row_ptr;
+//   3. one workgroup per pair: the same tests again, kept key blocks
 //      compacted in ascending order (wave ballots and a per-chunk prefix) and
-//      written as block indices and/or token-exact entry words (CSR) and as
-//      pair words.
+//      written as block indices and/or token-exact entry words.
 // Every thread tests its own candidates with closed-form rules, so a row
 // costs a few passes over nb candidates whatever its length.
 #include "internal.h"
@@ -102,49 +99,41 @@ __device__ inline void kept_by(const FrameCfg& c, const RowFrames& rf, const Row
   *k1 = rt.qb1 != rt.qb0 && keeps(c, rf, rt.b0, rt.b1, kb, P, B, N);
 }
 
-// Sums of three per-thread counts over the workgroup (thread 0's result).
-__device__ inline void block_sum3(int32_t (&v)[3], int32_t (*s_cnt)[kRowWaves]) {
-  for (int i = 0; i < 3; ++i) {
+// Sums of two per-thread counts over the workgroup (thread 0's result).
+__device__ inline void block_sum2(int32_t (&v)[2], int32_t (*s_cnt)[kRowWaves]) {
+  for (int i = 0; i < 2; ++i) {
     for (int off = 32; off > 0; off >>= 1) v[i] += __shfl_xor(v[i], off);
     if (threadIdx.x % 64 == 0) s_cnt[i][threadIdx.x / 64] = v[i];
   }
   __syncthreads();
   if (threadIdx.x == 0)
-    for (int i = 0; i < 3; ++i) {
+    for (int i = 0; i < 2; ++i) {
       v[i] = 0;
       for (int w = 0; w < kRowWaves; ++w) v[i] += s_cnt[i][w];
     }
 }
 
 __global__ __launch_bounds__(kRowThreads) void count_rows_kernel(
-    FrameCfg c, int32_t P, int32_t B, int32_t* __restrict__ row_ptr,
-    int32_t* __restrict__ pair_ptr) {
+    FrameCfg c, int32_t P, int32_t B, int32_t* __restrict__ row_ptr) {
   __shared__ RowFrames rf;
-  __shared__ int32_t s_cnt[3][kRowWaves];
+  __shared__ int32_t s_cnt[2][kRowWaves];
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
   const int32_t p = blockIdx.x;
   const RowTest rt = row_test(c, p, P, B, N, nb);
   load_row_frames(c, rt.qb0, rt.qb1, P, B, N, &rf);
-  int32_t cnt[3] = {0, 0, 0};   // row qb0, row qb1, pair row
+  int32_t cnt[2] = {0, 0};   // row qb0, row qb1
   for (int32_t kb = threadIdx.x; kb < nb; kb += kRowThreads) {
     bool k0, k1;
     kept_by(c, rf, rt, kb, P, B, N, &k0, &k1);
     cnt[0] += k0 ? 1 : 0;
     cnt[1] += k1 ? 1 : 0;
-    cnt[2] += (k0 || k1) ? 1 : 0;
   }
-  block_sum3(cnt, s_cnt);
+  block_sum2(cnt, s_cnt);
   if (threadIdx.x == 0) {
     row_ptr[rt.qb0 + 1] = cnt[0];
     if (rt.qb1 != rt.qb0) row_ptr[rt.qb1 + 1] = cnt[1];
-    pair_ptr[p + 1] = cnt[2];
-    if (p == 0) {
-      row_ptr[0] = 0;
-      pair_ptr[0] = 0;
-      // The attention kernel's work words after the offsets start at zero.
-      for (int i = 0; i < LVSA_PAIR_WORK; ++i) pair_ptr[gridDim.x + 1 + i] = 0;
-    }
+    if (p == 0) row_ptr[0] = 0;
   }
 }
 
@@ -174,35 +163,33 @@ __global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(int32_t rows,
 }
 
 // The CSR rows of the pair's query blocks (col_idx and/or entry words,
-// either may be null) and the pair row (pair words, in the token-exact form
-// when `exact`).
+// either may be null).
 __global__ __launch_bounds__(kRowThreads) void fill_rows_kernel(
     FrameCfg c, int32_t P, int32_t B, const int32_t* __restrict__ row_ptr,
-    int32_t* __restrict__ col_idx, uint32_t* __restrict__ entry,
-    const int32_t* __restrict__ pair_ptr, uint32_t* __restrict__ pair_words, bool exact) {
+    int32_t* __restrict__ col_idx, uint32_t* __restrict__ entry) {
   __shared__ RowFrames rf;
-  __shared__ int32_t s_wave[3][kRowWaves];
+  __shared__ int32_t s_wave[2][kRowWaves];
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
   const int32_t p = blockIdx.x;
   const RowTest rt = row_test(c, p, P, B, N, nb);
   load_row_frames(c, rt.qb0, rt.qb1, P, B, N, &rf);
   const int32_t lane = threadIdx.x % 64, wave = threadIdx.x / 64;
-  int32_t pos[3] = {row_ptr[rt.qb0], row_ptr[rt.qb1], pair_ptr[p]};
+  int32_t pos[2] = {row_ptr[rt.qb0], row_ptr[rt.qb1]};
   auto attends = [&](int32_t t, int32_t tau) { return seg_attends(c, rf, t, tau); };
   for (int32_t base = 0; base < nb; base += kRowThreads) {
     const int32_t kb = base + (int32_t)threadIdx.x;
     bool k0 = false, k1 = false;
     if (kb < nb) kept_by(c, rf, rt, kb, P, B, N, &k0, &k1);
-    const bool keep[3] = {k0, k1, k0 || k1};
-    int32_t at[3];
-    for (int i = 0; i < 3; ++i) {
+    const bool keep[2] = {k0, k1};
+    int32_t at[2];
+    for (int i = 0; i < 2; ++i) {
       const uint64_t bal = __ballot(keep[i]);
       at[i] = __popcll(bal & ((1ull << lane) - 1ull));
       if (lane == 0) s_wave[i][wave] = __popcll(bal);
     }
     __syncthreads();
-    for (int i = 0; i < 3; ++i) {
+    for (int i = 0; i < 2; ++i) {
       int32_t off = 0, total = 0;
       for (int w = 0; w < kRowWaves; ++w) {
         off += w < wave ? s_wave[i][w] : 0;
@@ -211,18 +198,14 @@ __global__ __launch_bounds__(kRowThreads) void fill_rows_kernel(
       at[i] += pos[i] + off;
       pos[i] += total;
     }
-    uint32_t e0 = 0u, e1 = 0u;
-    if (k0 && (entry || exact)) e0 = exact_entry(kb, rt.a0, rt.a1, c.T, P, B, N, attends);
-    if (k1 && (entry || exact)) e1 = exact_entry(kb, rt.b0, rt.b1, c.T, P, B, N, attends);
     if (k0) {
       if (col_idx) col_idx[at[0]] = kb;
-      if (entry) entry[at[0]] = e0;
+      if (entry) entry[at[0]] = exact_entry(kb, rt.a0, rt.a1, c.T, P, B, N, attends);
     }
     if (k1) {
       if (col_idx) col_idx[at[1]] = kb;
-      if (entry) entry[at[1]] = e1;
+      if (entry) entry[at[1]] = exact_entry(kb, rt.b0, rt.b1, c.T, P, B, N, attends);
     }
-    if (k0 || k1) pair_words[at[2]] = exact ? pair_exact_word(e0, e1) : pair_word_of(kb, k0, k1);
     __syncthreads();
   }
 }
@@ -236,18 +219,14 @@ bool device_mask_supported(const FrameCfg& c, int32_t P, int32_t B) {
 
 hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
-                                    uint32_t* d_entry, int32_t* d_pair_ptr,
-                                    uint32_t* d_pair_word, bool exact,
-                                    hipStream_t stream) {
+                                    uint32_t* d_entry, hipStream_t stream) {
   const int32_t nb = (int32_t)((mask_tokens(c, P) + B - 1) / B);
   const int32_t npairs = (nb + 1) / 2;
   hipLaunchKernelGGL(count_rows_kernel, dim3(npairs), dim3(kRowThreads), 0, stream, c, P, B,
-                     d_row_ptr, d_pair_ptr);
+                     d_row_ptr);
   hipLaunchKernelGGL(scan_rows_kernel, dim3(1), dim3(kScanThreads), 0, stream, nb, d_row_ptr);
-  hipLaunchKernelGGL(scan_rows_kernel, dim3(1), dim3(kScanThreads), 0, stream, npairs,
-                     d_pair_ptr);
   hipLaunchKernelGGL(fill_rows_kernel, dim3(npairs), dim3(kRowThreads), 0, stream, c, P, B,
-                     d_row_ptr, d_col_idx, d_entry, d_pair_ptr, d_pair_word, exact);
+                     d_row_ptr, d_col_idx, d_entry);
   return hipGetLastError();
 }
 

@@ -19,11 +19,7 @@
 //
 // The token-exact entry words (lvsa.h) are built alongside when asked for:
 // one word per kept block, from the two (at most) frames of each side.
-//
-// The attention kernel walks query blocks in pairs; build_pairs_host merges
-// each pair of CSR rows into the pair schedule it reads.
 #include <algorithm>
-#include <climits>
 #include <cstring>
 
 #include "internal.h"
@@ -110,82 +106,6 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
     std::memcpy(col_idx->data() + dst, uniq.data() + src[qb], len * sizeof(int32_t));
     if (entry)
       std::memcpy(entry->data() + dst, uniq_e.data() + src[qb], len * sizeof(uint32_t));
-  }
-}
-
-// Pair schedule: rows 2p and 2p+1 of the CSR merged (both ascending, no
-// repeats), each key block tagged with the rows that hold it.  Two passes
-// (row lengths, then the words into arrays of the final size); rows that are
-// equal, the common case (the two query blocks touch the same frames), are
-// copied with both tags instead of merged.
-void build_pairs_host(const std::vector<int32_t>& row_ptr,
-                      const std::vector<int32_t>& col_idx,
-                      const std::vector<uint32_t>* entry,
-                      std::vector<int32_t>* pair_ptr,
-                      std::vector<uint32_t>* pair_word,
-                      std::vector<uint32_t>* pair_exact) {
-  const int32_t nb = (int32_t)row_ptr.size() - 1;
-  const int32_t npairs = (nb + 1) / 2;
-  const bool exact = entry != nullptr && pair_exact != nullptr;
-  const int32_t* ci = col_idx.data();
-  // Rows of pair p: [i0, i1) and [k0, k1) (empty for the second row of an
-  // odd nb's last pair).
-  auto rows = [&](int32_t p, int64_t* i0, int64_t* i1, int64_t* k0, int64_t* k1) {
-    *i0 = row_ptr[2 * p];
-    *i1 = row_ptr[2 * p + 1];
-    *k0 = 2 * p + 1 < nb ? row_ptr[2 * p + 1] : 0;
-    *k1 = 2 * p + 1 < nb ? row_ptr[2 * p + 2] : 0;
-  };
-  auto same = [&](int64_t i0, int64_t i1, int64_t k0, int64_t k1) {
-    return k1 - k0 == i1 - i0 &&
-           std::memcmp(ci + i0, ci + k0, sizeof(int32_t) * (size_t)(i1 - i0)) == 0;
-  };
-  // Pass 1: row lengths.
-  pair_ptr->assign(npairs + 1, 0);
-  for (int32_t p = 0; p < npairs; ++p) {
-    int64_t i, ie, k, ke;
-    rows(p, &i, &ie, &k, &ke);
-    int64_t len = 0;
-    if (same(i, ie, k, ke)) {
-      len = ie - i;
-    } else {
-      while (i < ie && k < ke) {
-        const int32_t x = ci[i], y = ci[k];
-        i += x <= y;
-        k += y <= x;
-        ++len;
-      }
-      len += (ie - i) + (ke - k);
-    }
-    (*pair_ptr)[p + 1] = (*pair_ptr)[p] + (int32_t)len;
-  }
-  // Pass 2: the words.
-  pair_word->resize((size_t)(*pair_ptr)[npairs]);
-  if (exact) pair_exact->resize(pair_word->size());
-  uint32_t* w = pair_word->data();
-  uint32_t* we = exact ? pair_exact->data() : nullptr;
-  const uint32_t* en = exact ? entry->data() : nullptr;
-  for (int32_t p = 0; p < npairs; ++p) {
-    int64_t i, ie, k, ke;
-    rows(p, &i, &ie, &k, &ke);
-    int64_t o = (*pair_ptr)[p];
-    if (same(i, ie, k, ke)) {
-      for (int64_t n = 0; n < ie - i; ++n) w[o + n] = pair_word_of(ci[i + n], true, true);
-      if (exact)
-        for (int64_t n = 0; n < ie - i; ++n) we[o + n] = pair_exact_word(en[i + n], en[k + n]);
-      continue;
-    }
-    while (i < ie || k < ke) {
-      const int32_t x = i < ie ? ci[i] : INT32_MAX;
-      const int32_t y = k < ke ? ci[k] : INT32_MAX;
-      const int32_t kb = x < y ? x : y;
-      const bool in0 = x == kb, in1 = y == kb;
-      w[o] = pair_word_of(kb, in0, in1);
-      if (exact) we[o] = pair_exact_word(in0 ? en[i] : 0u, in1 ? en[k] : 0u);
-      ++o;
-      if (in0) ++i;
-      if (in1) ++k;
-    }
   }
 }
 

@@ -12,7 +12,6 @@ import pytest
 import paper_2605_31057_amd as L
 from paper_2605_31057_amd.inputs import WORKLOADS
 from oracle import mask as M
-from tests.pair_util import expected_pairs
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -30,7 +29,7 @@ def _declared_functions():
 def test_library_exports_every_declared_symbol():
     names = _declared_functions()
     assert {"lvsa_build_mask", "lvsa_attention", "lvsa_dense_attention",
-            "lvsa_build_mask_device", "lvsa_csr_pairs"} <= names
+            "lvsa_build_mask_device", "lvsa_csr_info", "lvsa_frame_window"} <= names
     lib = ctypes.CDLL(L.LIB_PATH)
     missing = [n for n in sorted(names) if not hasattr(lib, n)]
     assert not missing, missing
@@ -40,7 +39,7 @@ def test_status_strings_and_version():
     lib = L.lib()
     for s in (0, -1, -2, -3, -4, 7):
         assert lib.lvsa_status_str(s)
-    assert lib.lvsa_version() >= 100
+    assert lib.lvsa_version() >= 20000
     p = L.params_default()
     assert (p.budget_frames, p.window, p.tper, p.window_mode, p.rotate, p.tie_high,
             p.extra_anchors) == (21, 6, 0, L.WINDOW_EXPANDED, 1, 0, 0)
@@ -93,7 +92,8 @@ def test_host_builder_matches_oracle_rules(mode, rotate, tie_high):
     for _ in range(60):
         T = rng.randint(1, 40)
         W = rng.randint(0, 6)
-        tper = rng.randint(1, T)
+        # periods beyond T too (Eq. 3 then leaves one anchor, (s mod T_per) mod T)
+        tper = rng.randint(1, 3 * T)
         p = L.Params(window=W, tper=tper, window_mode=mode, rotate=rotate,
                      tie_high=tie_high, extra_anchors=rng.choice([0, 0, 1, 2, 5]))
         s = rng.randint(0, 3 * tper)
@@ -139,32 +139,62 @@ def _status(fn, *args):
     return fn(*args)
 
 
-PAIR_CASES = [  # T, P, B, step, text: even and odd nb, ragged tails, B = 64
-    (121, 1560, 128, 10, 0), (21, 1560, 128, 3, 0), (7, 300, 128, 1, 0),
-    (5, 200, 128, 0, 77), (9, 150, 64, 2, 0), (3, 50, 128, 0, 0), (1, 100, 128, 0, 0),
-]
+@pytest.mark.parametrize("T", [1, 2, 4, 7, 10])
+def test_anchor_period_longer_than_the_video(T):
+    """T_per > T (an explicit period): Eq. 3 keeps one anchor, (s mod T_per)
+    mod T, for every step up to 3 T_per; frame sets and CSR against the
+    oracle, and the anchor set against Eq. 3 written out."""
+    for tper in (T + 1, 2 * T, 3 * T, 100):
+        for s in range(0, 3 * tper + 1, max(1, tper // 7)):
+            p = L.Params(window=0, tper=tper)
+            _, anchors, _, _ = L.frame_sets(T, s, p)
+            assert anchors == [(s % tper) % T], (T, tper, s)
+            _check_frames(T, s, p)
+            _check_csr(T, 37, 16, s, p)
+            pe = L.Params(window=1, tper=tper, window_mode=L.WINDOW_EXPANDED, extra_anchors=1)
+            _check_frames(T, s, pe)
 
 
-@pytest.mark.parametrize("T,P,B,s,Lt", PAIR_CASES)
-def test_pair_schedule_merges_csr_rows(T, P, B, s, Lt):
-    """Bit for bit: the host pair schedule against its definition applied to
-    the oracle's CSR (block form) and to the handle's entry words (exact)."""
-    p = L.Params(text_tokens=Lt) if T >= 21 else L.Params(budget_frames=0, window=1,
-                                                          tper=3, text_tokens=Lt)
-    csr = L.build_mask(T, P, B, s, p, exact=P >= B)
-    want_rp, want_ci = M.build_mask(T, P, B, s, **_oracle_kw(p))
-    entry = csr.entries() if P >= B else None
-    ptr, words, exact = csr.pairs()
-    e_ptr, e_words, e_exact = expected_pairs(want_rp, want_ci, entry)
-    assert ptr.tolist() == e_ptr
-    assert words.tolist() == e_words
-    if entry is None:
-        assert exact is None
-    else:
-        assert exact.tolist() == e_exact
-    # Every pair row holds its two CSR rows (no block lost, none added).
-    nb = len(want_rp) - 1
-    assert len(ptr) == -(-nb // 2) + 1 and ptr[-1] <= len(want_ci)
+def test_csr_info_follows_the_boundary_order():
+    """lvsa_csr_info returns (n_q_blocks, n_kv_blocks, nnz, row_ptr, col_idx);
+    lvsa_csr_shape the tokens and the block size."""
+    T, P, B = 5, 200, 128
+    csr = L.build_mask(T, P, B, 1, L.Params(window=1, tper=3, text_tokens=77))
+    nq, nk, nnz, rp, ci = csr.info()
+    N = T * P + 77
+    assert nq == nk == -(-N // B)
+    assert csr.shape() == (N, B)
+    want_rp, want_ci = M.build_mask(T, P, B, 1, W=1, tper=3, text=77)
+    assert nnz == len(want_ci) == want_rp[-1]
+    assert [rp[i] for i in range(nq + 1)] == want_rp
+    assert [ci[i] for i in range(nnz)] == want_ci
+
+
+def test_frame_window_call_and_growth_match_alg1():
+    """The per-frame call equals the frame sets, and the growth counts equal
+    the iterations of Alg. 1 in the oracle, on the Wan and HV horizons and on
+    random rules."""
+    rng = random.Random(11)
+    cases = [(T, L.Params()) for T in (21, 41, 61, 81, 101, 121)]
+    cases += [(65, L.Params(budget_frames=33)), (129, L.Params(budget_frames=33))]
+    for _ in range(30):
+        T = rng.randint(1, 60)
+        cases.append((T, L.Params(window=rng.randint(0, 6), tper=rng.randint(1, 2 * T),
+                                  tie_high=rng.randint(0, 1),
+                                  extra_anchors=rng.choice([0, 1, 3]))))
+    for T, p in cases:
+        for s in (0, 3, 10, 17):
+            tper, anchors, lo, hi, grow = L.frame_sets(T, s, p, growth=True)
+            G = set(anchors)
+            for t in range(T):
+                assert L.frame_window(T, s, t, p) == (lo[t], hi[t], grow[t])
+                _, _, iters = M.expanded_window(t, G, p.window, T, bool(p.tie_high))
+                assert grow[t] == iters, (T, s, t)
+    with pytest.raises(L.LvsaError):
+        L.frame_window(21, 0, 21, L.Params())
+    # growth is 0 outside the expanded rule
+    assert set(L.frame_sets(121, 10, L.Params(window_mode=L.WINDOW_ADAPTIVE),
+                            growth=True)[4]) == {0}
 
 
 def test_invalid_mask_arguments():
@@ -196,7 +226,8 @@ def test_invalid_mask_arguments():
         assert out.value is None
     assert lib.lvsa_build_mask(121, 1560, 128, 0, 0, None, ref(out)) == L.EINVAL
     assert lib.lvsa_build_mask(121, 1560, 128, 0, 0, ref(good), None) == L.EINVAL
-    assert lib.lvsa_frame_sets(0, 0, ref(good), None, None, None, None, None) == L.EINVAL
+    assert lib.lvsa_frame_sets(0, 0, ref(good), None, None, None, None, None,
+                               None) == L.EINVAL
     lib.lvsa_csr_free(None)
 
 
@@ -205,15 +236,12 @@ def test_device_builder_rejects_before_launch():
     p = L.Params()
     fake = ctypes.c_void_p(0x1000)
     nb = 1475
-    pc = (nb + 1) // 2 * nb
-    build = lambda rp, ci, cap, pp, pw, pcap, step=0: lib.lvsa_build_mask_device(
-        121, 1560, 128, step, 0, ctypes.byref(p), rp, ci, cap, pp, pw, pcap, None)
-    assert build(fake, fake, nb * nb - 1, fake, fake, pc) == L.EINVAL   # CSR capacity
-    assert build(fake, fake, nb * nb, fake, fake, pc - 1) == L.EINVAL   # pair capacity
-    assert build(None, fake, nb * nb, fake, fake, pc) == L.EINVAL
-    assert build(fake, fake, nb * nb, None, fake, pc) == L.EINVAL
-    assert build(fake, fake, nb * nb, fake, None, pc) == L.EINVAL
-    assert build(fake, fake, nb * nb, fake, fake, pc, step=-3) == L.EINVAL
+    build = lambda rp, ci, cap, step=0: lib.lvsa_build_mask_device(
+        121, 1560, 128, step, 0, ctypes.byref(p), rp, ci, cap, None)
+    assert build(fake, fake, nb * nb - 1) == L.EINVAL   # CSR capacity
+    assert build(None, fake, nb * nb) == L.EINVAL
+    assert build(fake, None, nb * nb) == L.EINVAL
+    assert build(fake, fake, nb * nb, step=-3) == L.EINVAL
 
 
 def test_csr_device_view_requires_upload():
@@ -231,7 +259,7 @@ def test_attention_rejects_before_launch():
     lib = L.lib()
     ref = ctypes.byref
     nb = -(-1000 // 128)
-    m = L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0x5000, 0x6000)
+    m = L.BlockMask(1000, 128, nb, nb, 0x2000, 0x3000)
     q, k, v = _t(0x10000), _t(0x20000), _t(0x30000)
     o = _t(0x40000)
     cases = [
@@ -241,10 +269,11 @@ def test_attention_rejects_before_launch():
         (dict(q=_t(0x10008)), L.EUNSUPPORTED),           # alignment
         (dict(k=_t(0x20000, st=132)), L.EUNSUPPORTED),   # token stride % 8
         (dict(o=_t(0x10000)), L.EINVAL),                 # out aliases q
-        (dict(m=L.BlockMask(1000, 96, 11, 0x2000, 0x3000, 0x5000, 0x6000)), L.EUNSUPPORTED),
-        (dict(m=L.BlockMask(1000, 128, nb + 1, 0x2000, 0x3000, 0x5000, 0x6000)), L.EINVAL),
-        (dict(m=L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0, 0x6000)), L.EINVAL),
-        (dict(m=L.BlockMask(1000, 128, nb, 0x2000, 0x3000, 0x5000, 0)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 96, 11, 11, 0x2000, 0x3000)), L.EUNSUPPORTED),
+        (dict(m=L.BlockMask(1000, 128, nb + 1, nb + 1, 0x2000, 0x3000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 128, nb, nb - 1, 0x2000, 0x3000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 128, nb, nb, 0, 0x3000)), L.EINVAL),
+        (dict(m=L.BlockMask(1000, 128, nb, nb, 0x2000, 0)), L.EINVAL),
     ]
     for over, want in cases:
         a = dict(q=q, k=k, v=v, o=o, m=m)
@@ -359,22 +388,20 @@ def test_exact_attention_and_builder_reject_before_launch():
     p = L.Params()
     fake = ctypes.c_void_p(0x1000)
     nb = 1475
-    pc = (nb + 1) // 2 * nb
-    build = lambda P, rp, e, cap, pp, pw, pcap: lib.lvsa_build_exact_mask_device(
-        121, P, 128, 0, 0, ref(p), rp, e, cap, pp, pw, pcap, None)
-    assert build(1560, fake, fake, nb * nb - 1, fake, fake, pc) == L.EINVAL
-    assert build(1560, fake, fake, nb * nb, fake, fake, pc - 1) == L.EINVAL
-    assert build(100, fake, fake, 1 << 30, fake, fake, 1 << 30) == L.EUNSUPPORTED
-    assert build(1560, fake, None, nb * nb, fake, fake, pc) == L.EINVAL
-    assert build(1560, fake, fake, nb * nb, fake, None, pc) == L.EINVAL
+    build = lambda P, rp, e, cap: lib.lvsa_build_exact_mask_device(
+        121, P, 128, 0, 0, ref(p), rp, e, cap, None)
+    assert build(1560, fake, fake, nb * nb - 1) == L.EINVAL
+    assert build(100, fake, fake, 1 << 30) == L.EUNSUPPORTED
+    assert build(1560, fake, None, nb * nb) == L.EINVAL
+    assert build(1560, None, fake, nb * nb) == L.EINVAL
     n = 1000
     nbk = -(-n // 128)
     q, k, v, o = _t(0x10000), _t(0x20000), _t(0x30000), _t(0x40000)
-    em = lambda P, B, nb_, pw=0x6000: L.ExactMask(n, B, nb_, P, 0x2000, 0x3000, 0x5000, pw)
+    em = lambda P, B, nb_, e=0x3000: L.ExactMask(n, B, nb_, P, 0x2000, e)
     cases = [
         (em(100, 128, nbk), L.EUNSUPPORTED),        # P < B
         (em(0, 128, nbk), L.EINVAL),                # P < 1
-        (em(200, 128, nbk, pw=0), L.EINVAL),        # no pair words
+        (em(200, 128, nbk, e=0), L.EINVAL),         # no entry words
         (em(200, 96, 11), L.EUNSUPPORTED),          # block
     ]
     for m, want in cases:
@@ -424,21 +451,3 @@ def test_host_builder_text_on_hv_horizon():
     out = ctypes.c_void_p()
     assert L.lib().lvsa_build_mask(65, 1590, 128, 0, 0, ctypes.byref(bad),
                                    ctypes.byref(out)) == L.EINVAL
-
-
-def test_device_builder_binding_rejects_short_pair_ptr():
-    """The device pair_ptr carries PAIR_WORK work words after its offsets; the
-    binding refuses a buffer without them before any library call."""
-    import torch
-    T, P, B = 4, 256, 64
-    nb = -(-T * P // B)
-    npairs = (nb + 1) // 2
-    rp = torch.empty(nb + 1, dtype=torch.int32)
-    ci = torch.empty(nb * nb, dtype=torch.int32)
-    pw = torch.empty(npairs * nb, dtype=torch.int32)
-    p = L.Params(budget_frames=2, window=0, tper=4)
-    for build, second in ((L.build_mask_device, ci), (L.build_exact_mask_device, ci)):
-        with pytest.raises(L.LvsaError) as e:
-            build(T, P, B, 0, rp, second, params=p,
-                  pair_ptr=torch.empty(npairs + 1, dtype=torch.int32), pair_word=pw)
-        assert e.value.status == L.EINVAL

@@ -13,7 +13,6 @@ from paper_2605_31057_amd.inputs import WORKLOADS, make_qkv
 from oracle import attention as OA
 from oracle import mask as M
 from tests.gpu_util import assert_close
-from tests.pair_util import expected_pairs
 
 pytestmark = pytest.mark.gpu
 
@@ -29,22 +28,11 @@ def _device_csr(T, P, B, step, p, layer=0):
     nb = -(-(T * P + p.text_tokens) // B)
     rp = torch.full((nb + 1,), -1, dtype=torch.int32, device="cuda")
     ci = torch.full((nb * nb,), -1, dtype=torch.int32, device="cuda")
-    npairs = (nb + 1) // 2
-    pp = torch.full((npairs + 1 + L.PAIR_WORK,), -1, dtype=torch.int32, device="cuda")
-    pw = torch.full(((nb + 1) // 2 * nb,), -1, dtype=torch.int32, device="cuda")
-    L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer, pair_ptr=pp,
-                        pair_word=pw)
+    L.build_mask_device(T, P, B, step, rp, ci, params=p, layer=layer)
     torch.cuda.synchronize()
     rp = rp.cpu()
     nnz = int(rp[-1])
-    pp = pp.cpu()
-    # the attention kernels' work words after the offsets are zeroed
-    assert bool((pp[npairs + 1:] == 0).all())
-    pp = pp[:npairs + 1]
-    words = pw[:int(pp[-1])].cpu().numpy().view(np.uint32)
-    # nothing written past the pair words either
-    assert bool((pw[int(pp[-1]):] == -1).all())
-    return rp.tolist(), ci[:nnz].cpu().tolist(), ci, (pp.tolist(), words.tolist())
+    return rp.tolist(), ci[:nnz].cpu().tolist(), ci
 
 
 def _kw(p):
@@ -62,14 +50,11 @@ def test_device_builder_matches_oracle_workloads(name):
     print(f"[mask] {name} steps {steps[0]}..{steps[-1]}", flush=True)
     for s in steps:
         for layer in w.layers:
-            rp, ci, raw, (pp, pw) = _device_csr(w.frames, w.tokens_per_frame, w.block, s,
-                                                p, layer)
+            rp, ci, raw = _device_csr(w.frames, w.tokens_per_frame, w.block, s, p, layer)
             want_rp, want_ci = M.build_mask(w.frames, w.tokens_per_frame, w.block, s,
                                             layer=layer, **_kw(p))
             assert rp == want_rp, (name, s, layer)
             assert ci == want_ci, (name, s, layer)
-            e_pp, e_pw, _ = expected_pairs(want_rp, want_ci)
-            assert pp == e_pp and pw == e_pw, (name, s, layer)
             # nothing written past nnz
             assert bool((raw[len(ci):] == -1).all())
 
@@ -80,19 +65,18 @@ def test_device_builder_matches_oracle_random(mode):
     print(f"[mask] random mode {mode}", flush=True)
     for _ in range(40):
         T = rng.randint(1, 60)
-        p = L.Params(window=rng.randint(0, 6), tper=rng.randint(1, T), window_mode=mode,
+        # periods beyond T too (one anchor, (s mod T_per) mod T)
+        p = L.Params(window=rng.randint(0, 6), tper=rng.randint(1, 3 * T), window_mode=mode,
                      rotate=rng.randint(0, 1), tie_high=rng.randint(0, 1),
                      extra_anchors=rng.choice([0, 0, 1, 3]))
         P = rng.randint(1, 300)
         B = rng.choice([1, 3, 16, 64, 128])
         if -(-(T * P) // B) > 1500:
             B = 64
-        s = rng.randint(0, 40)
-        rp, ci, _, (pp, pw) = _device_csr(T, P, B, s, p)
+        s = rng.randint(0, 3 * p.tper)
+        rp, ci, _ = _device_csr(T, P, B, s, p)
         want_rp, want_ci = M.build_mask(T, P, B, s, **_kw(p))
         assert rp == want_rp and ci == want_ci, (T, P, B, s)
-        e_pp, e_pw, _ = expected_pairs(want_rp, want_ci)
-        assert pp == e_pp and pw == e_pw, (T, P, B, s)
 
 
 def test_device_mask_attention_equals_host_mask_attention():
@@ -137,9 +121,8 @@ def test_pattern_variant_attention_parity(mode, rotate, extra):
     for s in (1, 2):
         kw = _kw(p)
         rp, ci = M.build_mask(T, P, B, s, **kw)
-        drp, dci, _, (dpp, dpw) = _device_csr(T, P, B, s, p)
+        drp, dci, _ = _device_csr(T, P, B, s, p)
         assert drp == rp and dci == ci
-        assert (dpp, dpw) == expected_pairs(rp, ci)[:2]
         csr = L.build_mask(T, P, B, s, p, exact=True)
         csr.upload()
         blk = L.attention(qd, kd, vd, csr.device_mask())
