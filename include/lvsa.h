@@ -314,7 +314,8 @@ typedef struct lvsa_tensor {
  * block of i.  bf16 inputs, fp32 products and softmax, bf16 output (round to
  * nearest even).  q, k, v, out share heads, n_tokens = mask->n_tokens and
  * head_dim = 128; mask->block is 64 or 128 and mask->n_q_blocks =
- * mask->n_kv_blocks = ceil(N / B).  Rows i >= N of `out` are never written;
+ * mask->n_kv_blocks = ceil(N / B) <= 8000 (a workgroup merges the two CSR
+ * rows of its pair of query blocks in LDS).  Rows i >= N of `out` are never written;
  * a query block whose row is empty gets zeros.  out must not overlap q, k or
  * v.  The result is deterministic (fixed key order per row, whichever
  * workgroup computes it).
@@ -327,8 +328,9 @@ lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
 /* Token-exact attention forward (Eq. 2 token for token): as lvsa_attention,
  * with the keys of each kept block further restricted, per query token, by
  * the block's entry word, so query i attends exactly the keys j with
- * frame(j) in A(frame(i)).  mask->block is 64 or 128 and mask->frame_tokens
- * >= mask->block; every query token keeps at least its own frame's keys.
+ * frame(j) in A(frame(i)).  mask->block is 64 or 128, mask->frame_tokens
+ * >= mask->block and mask->n_q_blocks <= 8000; every query token keeps at
+ * least its own frame's keys.
  * Errors as for lvsa_attention. */
 lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  const lvsa_tensor* v,

@@ -543,6 +543,7 @@ lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            lvsa_tensor* out, void* stream) {
   if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
   if (mask->n_kv_blocks != mask->n_q_blocks) return LVSA_EINVAL;
+  if (mask->n_q_blocks > kMaxSparseBlocks) return LVSA_EUNSUPPORTED;
   AttnArgs a;
   const lvsa_status st = attention_args(q, k, v, mask->n_tokens, mask->block,
                                         mask->n_q_blocks, out, &a);
@@ -558,7 +559,8 @@ lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  void* stream) {
   if (!mask || !mask->row_ptr || !mask->entry) return LVSA_EINVAL;
   if (mask->frame_tokens < 1) return LVSA_EINVAL;
-  if (!exact_supported(mask->frame_tokens, mask->block, mask->n_q_blocks))
+  if (!exact_supported(mask->frame_tokens, mask->block, mask->n_q_blocks) ||
+      mask->n_q_blocks > kMaxSparseBlocks)
     return LVSA_EUNSUPPORTED;
   AttnArgs a;
   const lvsa_status st = attention_args(q, k, v, mask->n_tokens, mask->block,

@@ -17,14 +17,15 @@
 //   compute unit takes tiles through atomic counters (fetch_tile).
 //
 // The merged walk
-//   CSR rows 2p and 2p+1 are walked from their last entries down: each step
-//   takes the larger of the two rows' next entries (both, when they are
-//   equal), so the step's key block comes with a flag per query block and
-//   the key blocks come in descending order, each once.  The merge is scalar
-//   arithmetic, repeated in every wave, on two candidate entries that one
-//   vector load (lanes 0 and 1) fetches at the start of the step whose end
-//   consumes them; merges run three steps ahead of the step that uses their
-//   key block, because K tiles are loaded two steps ahead.  The mask is only
+//   A tile's key blocks are the union of CSR rows 2p and 2p+1, walked in
+//   descending order, each key block once with a flag per query block.  At
+//   the start of the tile the workgroup merges the two rows in LDS: every
+//   entry's position in the union is its index in its own row plus the
+//   entries of the other row above it (a binary search) minus the entries
+//   above it that both rows hold (a ballot count), and the step words are
+//   written there.  The step loop then reads one word per step, three steps
+//   ahead (K tiles are loaded two steps ahead).  Rows longer than WALK_CAP
+//   are merged WALK_CAP words at a time between steps.  The mask is only
 //   read, so any number of launches can share it.
 //
 // Schedule ("ping-pong", one key block per step)
@@ -449,43 +450,127 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
   }
 }
 
-// Walk over CSR rows 2p ("row 0") and 2p+1 ("row 1") of a mask, from their
-// last entries down (see "The merged walk" above).  Row 1 starts where row 0
-// ends, so row 0's first entry is also the first entry of the pair.
-struct PairWalk {
-  int32_t i0, i1;     // next entry of row 0 / row 1 (walking down)
-  int32_t lo0, lo1;   // first entry of row 0 / row 1; a row is done below it
-  int32_t n;          // step words produced so far
+// LDS of the merged walk: the step words of the tile's pair of query blocks
+// (kept for the whole tile) and per-wave counts of the merge.  The merge's
+// inputs, the two CSR rows, are staged in the K/V tile buffers, which are
+// idle at the start of a tile.  A pair's union has at most nb words, so
+// nb <= WALK_CAP (checked before launch) lets one merge cover the tile.
+constexpr int WALK_CAP = 8000;
+struct WalkLds {
+  uint32_t w[WALK_CAP];       // step words, in walk order
+  int32_t cnt[2][16][5];      // per-wave counts of a merge pass (double-buffered)
 };
+static_assert(2 * WALK_CAP * 4 <= 4 * Tile<64>::BYTES, "rows staged in the tile buffers");
 
-// Step word of the next key block of the walk, from the candidates a (row
-// 0's entry i0) and b (row 1's entry i1); `prev` again when both rows are
-// done.  Block form (row entries are key blocks): kb in bits 0..29, bit 30 /
-// 31 set when row 0 / row 1 keeps it.  Token-exact form (row entries are
-// entry words): bits 0..23 kb and kfirst, bits 24..27 / 28..31 the patterns
-// of row 0 / row 1, 0 where that row does not keep kb.  A key block outside
-// [0, nb) costs a step that masks every key.
-template <int MODE>
-__device__ __forceinline__ uint32_t walk_next(PairWalk& pw, uint32_t a, uint32_t b,
-                                              uint32_t prev, int32_t nb) {
-  constexpr bool EXACT = MODE == ATTN_EXACT;
-  const int32_t ka = pw.i0 >= pw.lo0 ? (EXACT ? (int32_t)(a & 0xFFFFu) : (int32_t)a) : -1;
-  const int32_t kc = pw.i1 >= pw.lo1 ? (EXACT ? (int32_t)(b & 0xFFFFu) : (int32_t)b) : -1;
-  const int32_t kb = ka > kc ? ka : kc;
-  if (kb < 0) return prev;
-  const bool in0 = ka == kb, in1 = kc == kb;
-  pw.i0 -= in0 ? 1 : 0;
-  pw.i1 -= in1 ? 1 : 0;
-  pw.n += 1;
-  if (kb >= nb) return EXACT ? 0xFFFFu : 0x3FFFFFFFu;
-  if constexpr (EXACT) {
-    const uint32_t base = (in0 ? a : b) & 0xFFFFFFu;
-    return base | (in0 ? a & 0x0F000000u : 0u) | (in1 ? (b & 0x0F000000u) << 4 : 0u);
-  }
+// Step words.  Block form (row entries are key blocks): kb in bits 0..29,
+// bit 30 / 31 set when row 0 / row 1 keeps kb.  Token-exact form (row
+// entries are entry words): bits 0..23 kb and kfirst, bits 24..27 / 28..31
+// the patterns of row 0 / row 1, 0 where that row does not keep kb.  A key
+// block outside [0, nb) gives a word that masks every key (and whose loads
+// read zeros).
+template <bool EXACT>
+__device__ __forceinline__ int32_t entry_key(uint32_t e) {
+  return EXACT ? (int32_t)(e & 0xFFFFu) : (int32_t)e;
+}
+template <bool EXACT>
+__device__ __forceinline__ uint32_t step_word(uint32_t e0, uint32_t e1, bool in0, bool in1,
+                                              int32_t nb) {
+  const int32_t kb = entry_key<EXACT>(in0 ? e0 : e1);
+  if (kb < 0 || kb >= nb) return EXACT ? 0xFFFFu : 0x3FFFFFFFu;
+  if constexpr (EXACT)
+    return ((in0 ? e0 : e1) & 0xFFFFFFu) | (in0 ? e0 & 0x0F000000u : 0u) |
+           (in1 ? (e1 & 0x0F000000u) << 4 : 0u);
   return (uint32_t)kb | (in0 ? 1u << 30 : 0u) | (in1 ? 1u << 31 : 0u);
 }
 
-typedef const __attribute__((address_space(1))) uint32_t global_u32;
+// Merges CSR rows 2p ("row 0": entries lo0 .. hi0-1) and 2p+1 ("row 1":
+// lo1 .. hi1-1) into L.w, largest key first (every thread of the workgroup
+// takes part; starts and ends with a barrier).  Both rows are staged in
+// `stage` from their ends down; an entry's position in the union is its
+// index in its own row, plus the entries of the other row with a larger key
+// (a binary search), minus the keys above it that both rows hold (a count of
+// its row's duplicates before it).  Returns the number of words.  Rows of up
+// to WALK_CAP entries are merged whole (more are cut); rows that are not
+// strictly ascending give some order of their entries, never a write outside
+// L.w.
+template <int NT, bool EXACT>
+__device__ __forceinline__ int32_t merge_pair(WalkLds& L, uint32_t* stage,
+                                              const uint32_t* __restrict__ rows,
+                                              int32_t lo0, int32_t hi0, int32_t lo1,
+                                              int32_t hi1, int32_t nb) {
+  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  constexpr int NWAVE = NT / 64;
+  uint32_t* const sa = stage;              // row 0, largest key first
+  uint32_t* const sb = stage + WALK_CAP;   // row 1
+  const int na = max(0, min(hi0 - lo0, WALK_CAP));
+  const int nc = max(0, min(hi1 - lo1, WALK_CAP));
+  __syncthreads();   // the stage buffers are idle
+  for (int t = tid; t < na; t += NT) sa[t] = rows[hi0 - 1 - t];
+  for (int t = tid; t < nc; t += NT) sb[t] = rows[hi1 - 1 - t];
+  __syncthreads();
+  int dup_base0 = 0, dup_base1 = 0, words = 0;
+  const int passes = (max(na, nc) + NT - 1) / NT;
+  for (int ps = 0; ps < passes; ++ps) {
+    const int t = ps * NT + tid;
+    // Entries of the other row with a larger key: the first index whose key
+    // is not larger (the staged rows descend), by binary search.
+    int above0 = 0, above1 = 0;
+    bool dup0 = false, dup1 = false;
+    uint32_t e0 = 0u, e1 = 0u, p0 = 0u;
+    if (t < na) {
+      e0 = sa[t];
+      const int32_t x = entry_key<EXACT>(e0);
+      int lo = 0, hi = nc;
+      while (lo < hi) {
+        const int mid = (lo + hi) / 2;
+        if (entry_key<EXACT>(sb[mid]) > x) lo = mid + 1; else hi = mid;
+      }
+      above0 = lo;
+      if (lo < nc) {
+        p0 = sb[lo];
+        dup0 = entry_key<EXACT>(p0) == x;
+      }
+    }
+    if (t < nc) {
+      e1 = sb[t];
+      const int32_t y = entry_key<EXACT>(e1);
+      int lo = 0, hi = na;
+      while (lo < hi) {
+        const int mid = (lo + hi) / 2;
+        if (entry_key<EXACT>(sa[mid]) > y) lo = mid + 1; else hi = mid;
+      }
+      above1 = lo;
+      dup1 = lo < na && entry_key<EXACT>(sa[lo]) == y;
+    }
+    // Keys held by both rows above each entry: its row's duplicates before it.
+    const uint64_t m0 = __ballot(dup0), m1 = __ballot(dup1);
+    const uint64_t below = (1ull << lane) - 1ull;
+    if (lane == 0) {
+      L.cnt[ps & 1][wave][0] = __popcll(m0);
+      L.cnt[ps & 1][wave][1] = __popcll(m1);
+    }
+    __syncthreads();
+    int before0 = dup_base0 + __popcll(m0 & below), before1 = dup_base1 + __popcll(m1 & below);
+    for (int w = 0; w < NWAVE; ++w) {
+      const int v0 = L.cnt[ps & 1][w][0], v1 = L.cnt[ps & 1][w][1];
+      before0 += w < wave ? v0 : 0;
+      before1 += w < wave ? v1 : 0;
+      dup_base0 += v0;
+      dup_base1 += v1;
+    }
+    if (t < na) {
+      const int r = t + above0 - before0;
+      if (r >= 0 && r < WALK_CAP) L.w[r] = step_word<EXACT>(e0, p0, true, dup0, nb);
+    }
+    if (t < nc && !dup1) {
+      const int r = t + above1 - before1;
+      if (r >= 0 && r < WALK_CAP) L.w[r] = step_word<EXACT>(0u, e1, false, true, nb);
+    }
+    words = na + nc - dup_base1;
+  }
+  __syncthreads();   // the words are written; the stage buffers are free again
+  return __builtin_amdgcn_readfirstlane(min(words, WALK_CAP));
+}
 
 // MODE: ATTN_DENSE (every key block), ATTN_BLOCK (CSR rows of key blocks),
 // ATTN_EXACT (CSR rows of token-exact entry words).
@@ -493,7 +578,7 @@ typedef const __attribute__((address_space(1))) uint32_t global_u32;
 // using the workgroup's LDS stages `lds` (K slots 0-1, V slots 0-1).
 template <int BLOCK, int MODE>
 __device__ __forceinline__ void attn_tile(
-    char* lds, int tile, const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
+    char* lds, WalkLds& walk, int tile, const __bf16* __restrict__ qg, const __bf16* __restrict__ kg,
     const __bf16* __restrict__ vg, __bf16* __restrict__ og, int64_t q_sh,
     int64_t q_st, int64_t k_sh, int64_t k_st, int64_t v_sh, int64_t v_st,
     int64_t o_sh, int64_t o_st, int32_t H, int32_t N, int32_t nb,
@@ -571,56 +656,27 @@ __device__ __forceinline__ void attn_tile(
       mask_tail<BLOCK>(sc, lane, ((w >> kept_bit) & 1u) ? N - kb * BLOCK : 0);
   };
 
-  // The walk (sparse modes) or the key blocks nb-1 .. 0 (dense).  Words of
-  // steps past the last one repeat it: their loads land in slots that no
-  // later step reads.  Every row entry the walk loads is an entry of the
-  // pair (an exhausted row's lane reads the pair's first entry instead), so
-  // no load leaves the mask's arrays.
-  PairWalk pw{};
+  // The walk (sparse modes) or the key blocks nb-1 .. 0 (dense): n steps.
+  // Words of steps past the last one repeat it: their loads land in slots
+  // that no later step reads.
+  int n = nb;
   uint32_t w0 = 0u, w1 = 0u, w2 = 0u;
-  global_u32* const rg = (global_u32*)rows;
   if constexpr (SPARSE) {
     const int32_t r0 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq]);
     const int32_t r1 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 1]);
     const int32_t r2 =
         2 * pq + 1 < nb ? __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 2]) : r1;
-    pw.lo0 = r0;
-    pw.i0 = r1 - 1;
-    pw.lo1 = r1;
-    pw.i1 = r2 - 1;
-    if (r0 < r2) {
-      // The first three merges read at most the last three entries of each
-      // row: one load, lanes 0..2 row 0 from its end, lanes 3..5 row 1.
-      const int32_t want = lane < 3 ? pw.i0 - lane : pw.i1 - (lane - 3);
-      const int32_t from = lane < 3 ? pw.lo0 : pw.lo1;
-      const uint32_t first = rg[want >= from ? want : r0];
-      auto cand = [&](int row) {
-        const int32_t used = row == 0 ? r1 - 1 - pw.i0 : r2 - 1 - pw.i1;
-        return (uint32_t)__builtin_amdgcn_readlane((int)first, 3 * row + min(used, 2));
-      };
-      w0 = walk_next<MODE>(pw, cand(0), cand(1), 0u, nb);
-      w1 = walk_next<MODE>(pw, cand(0), cand(1), w0, nb);
-      w2 = walk_next<MODE>(pw, cand(0), cand(1), w1, nb);
+    n = merge_pair<TL::NT, EXACT>(walk, (uint32_t*)lds, rows, r0, r1, r1, r2, nb);
+    if (n > 0) {
+      w0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[0]);
+      w1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(1, n - 1)]);
+      w2 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(2, n - 1)]);
     }
   } else {
-    pw.n = nb;
     w0 = (uint32_t)(nb - 1) | 0xC0000000u;
     w1 = (uint32_t)max(nb - 2, 0) | 0xC0000000u;
     w2 = (uint32_t)max(nb - 3, 0) | 0xC0000000u;
   }
-  // Candidates of the merge at the end of a step: lane 0 row 0's entry i0,
-  // lane 1 row 1's entry i1.  A vector load, so that its wait is the step's
-  // final vmcnt(0) rather than the next LDS wait, whose counter a scalar load
-  // would share.
-  auto fetch_candidates = [&]() -> uint32_t {
-    if constexpr (SPARSE) {
-      const int32_t i0 = pw.i0 >= pw.lo0 ? pw.i0 : pw.lo0;
-      const int32_t i1 = pw.i1 >= pw.lo1 ? pw.i1 : pw.lo0;
-      return rg[lane == 0 ? i0 : i1];
-    } else {
-      return 0u;
-    }
-  };
 
   WaveState ws;
 #pragma unroll
@@ -638,7 +694,7 @@ __device__ __forceinline__ void attn_tile(
     for (int e = 0; e < 8; ++e) ones[e] = one ? (__bf16)1.f : (__bf16)0.f;
   }
 
-  if (pw.n > 0) {
+  if (n > 0) {
     // LDS stages: K(b) in K slot b % 2, V(b) in V slot b % 2.
     const uint32_t k_slot0 = lds_base, v_slot0 = lds_base + 2 * TL::BYTES;
     const char* const k_lds = lds;
@@ -664,8 +720,11 @@ __device__ __forceinline__ void attn_tile(
     Probs<BLOCK> pr;
     if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
     __syncthreads();
-    for (int j = 0; j < pw.n; ++j) {
-      const uint32_t cv = fetch_candidates();
+    for (int j = 0; j < n; ++j) {
+      // Word of step j+3 from the walk's LDS, read now and used at the end of
+      // the step (the last word again past the end of the walk).
+      uint32_t w3v = 0u;
+      if constexpr (SPARSE) w3v = walk.w[min(j + 3, n - 1)];
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
@@ -682,21 +741,15 @@ __device__ __forceinline__ void attn_tile(
       __syncthreads();
       // half-period 2j+1
       if (lead) {
-        if (j + 1 < pw.n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
+        if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
       } else {
         gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
         mask_block(sc, w1);
       }
       wait_loads_and_sync();
-      uint32_t w3;
-      if constexpr (SPARSE) {
-        w3 = walk_next<MODE>(pw, (uint32_t)__builtin_amdgcn_readlane((int)cv, 0),
-                             (uint32_t)__builtin_amdgcn_readlane((int)cv, 1), w2, nb);
-      } else {
-        w3 = (uint32_t)max(nb - 4 - j, 0) | 0xC0000000u;
-      }
       w1 = w2;
-      w2 = w3;
+      w2 = SPARSE ? (uint32_t)__builtin_amdgcn_readfirstlane((int)w3v)
+                  : (uint32_t)max(nb - 4 - j, 0) | 0xC0000000u;
     }
     __syncthreads();
   }
@@ -775,8 +828,9 @@ struct KArgs {
 };
 
 template <int BLOCK, int MODE>
-__device__ __forceinline__ void attn_tile_args(char* lds, int tile, const KArgs& a) {
-  attn_tile<BLOCK, MODE>(lds, tile, a.q, a.k, a.v, a.o, a.q_sh, a.q_st, a.k_sh, a.k_st,
+__device__ __forceinline__ void attn_tile_args(char* lds, WalkLds& walk, int tile,
+                                               const KArgs& a) {
+  attn_tile<BLOCK, MODE>(lds, walk, tile, a.q, a.k, a.v, a.o, a.q_sh, a.q_st, a.k_sh, a.k_st,
                          a.v_sh, a.v_st, a.o_sh, a.o_st, a.H, a.N, a.nb, a.row_ptr,
                          a.rows, a.P, a.scale_log2);
 }
@@ -787,6 +841,7 @@ __device__ __forceinline__ void attn_tile_args(char* lds, int tile, const KArgs&
 template <int BLOCK, int MODE>
 __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(const KArgs args) {
   __shared__ __attribute__((aligned(1024))) char lds[4 * Tile<BLOCK>::BYTES];
+  __shared__ WalkLds walk;
   __shared__ int next_tile;
   const int total = (args.nb + 1) / 2 * args.H;
   // Workgroups are dispatched round-robin over the 8 XCDs.
@@ -804,7 +859,7 @@ __global__ __launch_bounds__(Tile<BLOCK>::NT) void attn_fwd_kernel(const KArgs a
     asm volatile("" : "+v"(zero));
     zero = __builtin_amdgcn_readfirstlane(zero);
     const KArgs* ap = (const KArgs*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() + zero);
-    attn_tile_args<BLOCK, MODE>(lds, tile, *ap);
+    attn_tile_args<BLOCK, MODE>(lds, walk, tile, *ap);
   }
 }
 
@@ -831,8 +886,8 @@ template <int BLOCK, int MODE>
 hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
   const float scale_log2 = 1.4426950408889634f / __builtin_sqrtf((float)D);
   const int tiles = (a.n_blocks + 1) / 2 * a.heads;
-  // One persistent workgroup per CU (each takes 128 KB of LDS, so one fits
-  // a CU), or one per tile when there are fewer tiles.
+  // One persistent workgroup per CU (each takes 160 KB of LDS at BLOCK =
+  // 128, so one fits a CU), or one per tile when there are fewer tiles.
   const int grid = tiles < cu_count() ? tiles : cu_count();
   KArgs k;
   k.q = (const __bf16*)a.q;

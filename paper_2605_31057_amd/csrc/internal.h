@@ -41,6 +41,10 @@ hipError_t launch_build_mask_device(const FrameCfg& c, int32_t P, int32_t B,
                                     int32_t* d_row_ptr, int32_t* d_col_idx,
                                     uint32_t* d_entry, hipStream_t stream);
 
+// Key blocks a sparse attention launch supports: a workgroup merges the two
+// CSR rows of its pair of query blocks (at most nb words) in LDS.
+constexpr int32_t kMaxSparseBlocks = 8000;
+
 // Tile counters of one attention launch: eight 64-bit words (one per XCD),
 // zeroed on the launch stream before the kernel runs.
 constexpr int kTileCounters = 8;
