@@ -325,6 +325,21 @@ lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                            const lvsa_tensor* v, const lvsa_block_mask* mask,
                            lvsa_tensor* out, void* stream);
 
+/* lvsa_attention without any allocation, for callers that cannot allocate
+ * device memory (code under graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same kernels and results, with the tile
+ * counters taken from a fixed array in the library's device data (one set
+ * of counters, 64 bytes per device, enough for every launch lvsa_attention
+ * accepts; the shape limits are the same).  It allocates nothing and issues
+ * no memset: the counters are zeroed by a kernel on `stream`.  All calls on
+ * one device share that array, so calls that overlap in time on one device
+ * (on two streams, or from two threads) race; successive calls on one
+ * stream are fine.  Errors as for lvsa_attention (EDEVICE when the array's
+ * device address cannot be looked up). */
+lvsa_status lvsa_attention_noalloc(const lvsa_tensor* q, const lvsa_tensor* k,
+                                   const lvsa_tensor* v, const lvsa_block_mask* mask,
+                                   lvsa_tensor* out, void* stream);
+
 /* Token-exact attention forward (Eq. 2 token for token): as lvsa_attention,
  * with the keys of each kept block further restricted, per query token, by
  * the block's entry word, so query i attends exactly the keys j with

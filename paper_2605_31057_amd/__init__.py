@@ -23,7 +23,8 @@ import os
 __all__ = [
     "LvsaError", "Params", "Csr", "BlockMask", "ExactMask", "lib",
     "params_default", "frame_sets", "frame_window", "build_mask", "build_mask_device",
-    "build_exact_mask_device", "csr_mask", "attention", "attention_exact",
+    "build_exact_mask_device", "csr_mask", "attention", "attention_noalloc",
+    "attention_exact",
     "dense_attention", "WINDOW_BASIC", "WINDOW_ADAPTIVE", "WINDOW_EXPANDED",
     "MAX_FRAMES",
 ]
@@ -126,6 +127,9 @@ def lib():
                                       ctypes.POINTER(_Tensor), _p]),
             "lvsa_attention": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
                                [ctypes.POINTER(BlockMask), ctypes.POINTER(_Tensor), _p]),
+            "lvsa_attention_noalloc": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
+                                       [ctypes.POINTER(BlockMask), ctypes.POINTER(_Tensor),
+                                        _p]),
             "lvsa_dense_attention": (_i32, [ctypes.POINTER(_Tensor)] * 3 +
                                      [_i32, ctypes.POINTER(_Tensor), _p]),
         }
@@ -352,6 +356,17 @@ def attention(q, k, v, mask, out=None, stream=None):
     _check(lib().lvsa_attention(ctypes.byref(tq), ctypes.byref(tk), ctypes.byref(tv),
                                 ctypes.byref(mask), ctypes.byref(to),
                                 _stream_ptr(stream)), "lvsa_attention")
+    return out
+
+
+def attention_noalloc(q, k, v, mask, out, stream=None):
+    """lvsa_attention_noalloc: block-sparse attention that allocates nothing
+    (the caller passes `out`); calls overlapping on one device race."""
+    tq, tk, tv, to = (_tensor(x) for x in (q, k, v, out))
+    _check(lib().lvsa_attention_noalloc(ctypes.byref(tq), ctypes.byref(tk),
+                                        ctypes.byref(tv), ctypes.byref(mask),
+                                        ctypes.byref(to), _stream_ptr(stream)),
+           "lvsa_attention_noalloc")
     return out
 
 

@@ -165,6 +165,39 @@ void release_counters(const CounterLease& lease, hipStream_t stream) {
   if (hipEventRecord(cs.done, stream) != hipSuccess) cs.kept = true;
 }
 
+// Allocation-free launches (lvsa_attention_noalloc): the tile counters live
+// in a file-scope device array, one copy per device, whose device address is
+// looked up once per device (with that device current) and kept; the
+// array's name in host code is only a stand-in for the symbol, never a device
+// address.  Every such launch on a device uses the same counters, zeroed by
+// the launch's own zeroing kernel, so such launches must not overlap on a
+// device.
+constexpr int kNoAllocCounterSets = 1;
+static __device__ __align__(256) uint64_t scratch[kTileCounters * kNoAllocCounterSets];
+
+namespace {
+
+std::mutex g_scratch_mu;
+uint64_t* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of `scratch` (looked up on the first
+// call on a device, with that device current).
+lvsa_status noalloc_counters(uint64_t** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LVSA_EDEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+      return LVSA_EDEVICE;
+    g_scratch_ptr[dev] = (uint64_t*)ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return LVSA_OK;
+}
+
+}  // namespace
+
 }  // namespace lvsa
 
 struct lvsa_csr {
@@ -551,6 +584,24 @@ lvsa_status lvsa_attention(const lvsa_tensor* q, const lvsa_tensor* k,
   a.row_ptr = mask->row_ptr;
   a.rows = (const uint32_t*)mask->col_idx;
   return run_attention(a, mask->block, ATTN_BLOCK, stream);
+}
+
+lvsa_status lvsa_attention_noalloc(const lvsa_tensor* q, const lvsa_tensor* k,
+                                   const lvsa_tensor* v, const lvsa_block_mask* mask,
+                                   lvsa_tensor* out, void* stream) {
+  if (!mask || !mask->row_ptr || !mask->col_idx) return LVSA_EINVAL;
+  if (mask->n_kv_blocks != mask->n_q_blocks) return LVSA_EINVAL;
+  if (mask->n_q_blocks > kMaxSparseBlocks) return LVSA_EUNSUPPORTED;
+  AttnArgs a;
+  lvsa_status st = attention_args(q, k, v, mask->n_tokens, mask->block, mask->n_q_blocks,
+                                  out, &a);
+  if (st != LVSA_OK) return st;
+  a.row_ptr = mask->row_ptr;
+  a.rows = (const uint32_t*)mask->col_idx;
+  if ((st = noalloc_counters(&a.counters)) != LVSA_OK) return st;
+  if (launch_attention(a, mask->block, ATTN_BLOCK, (hipStream_t)stream) != hipSuccess)
+    return LVSA_EDEVICE;
+  return LVSA_OK;
 }
 
 lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
