@@ -65,6 +65,23 @@ def test_golden_windows():
     assert n >= 15
 
 
+def test_golden_attended_frames_basic_and_adaptive():
+    """A(t) through attended_frames for the basic and adaptive windows:
+    period, anchors (rotating, fixed, with a dedicated initial anchor) and
+    window together."""
+    modes = {"basic": M.WINDOW_BASIC, "adaptive": M.WINDOW_ADAPTIVE}
+    n = 0
+    for line in _lines("attended_frames.txt"):
+        lhs, rhs = line.split(":")
+        mode, rot, T, C, W, tper, E, s, t = lhs.split()
+        T, C, W, tper, E, s, t = map(int, (T, C, W, tper, E, s, t))
+        _, _, A = M.attended_frames(T, s, C=C, W=W, tper=tper, mode=modes[mode],
+                                    rotate=rot == "1", extra=E)
+        assert sorted(A[t]) == [int(x) for x in rhs.split()], line
+        n += 1
+    assert n >= 15
+
+
 def test_golden_tiny_mask():
     for line in _lines("tiny_mask.txt"):
         fields = [f.strip() for f in line.split("|")]
