@@ -84,9 +84,9 @@ def percentile(xs, q):
 
 def traffic_from_profile(workload, kernel):
     """HBM bytes per launch of `kernel` at `workload` from the committed PMC
-    summary of that workload (profiles/pmc_<workload>.json), if it was taken
+    summary of that workload (profiles/attn_pmc_<workload>.json), if it was taken
     on the current kernel source; else None."""
-    path = os.path.join(PROFILES, f"pmc_{workload}.json")
+    path = os.path.join(PROFILES, f"attn_pmc_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -209,9 +209,9 @@ def main():
     ap.add_argument("--no-patterns", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--pmc", action="store_true",
-                    help="counter-collection run: a few untimed sparse, dense and "
-                         "mask launches plus a 1 GiB copy (the byte-counter "
-                         "calibration), for rocprofv3 --pmc")
+                    help="counter-collection run: untimed block-sparse (3), token-exact "
+                         "(2) and dense (1) launches at step 10 plus three 1 GiB copies "
+                         "(the byte-counter calibration), for rocprofv3 --pmc")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -227,8 +227,17 @@ def main():
     w = WORKLOADS[args.workload]
     params = L.Params(budget_frames=w.budget_frames, window=w.window, tper=w.tper,
                       text_tokens=w.text_tokens)
-    print(f"[bench] {w.name}: generating inputs", file=sys.stderr, flush=True)
-    q, k, v = (x.cuda() for x in workload_qkv(w))
+    if args.pmc:
+        # Counter runs: the same shapes and value distribution drawn on the
+        # device from a seeded generator (counters do not depend on values,
+        # and drawing 40 heads on the host would dominate every pass).
+        g = torch.Generator(device="cuda")
+        g.manual_seed(16)
+        q, k, v = (torch.randn((w.heads, w.n_tokens, 128), generator=g, device="cuda")
+                   .mul_(w.value_scale).to(torch.bfloat16) for _ in range(3))
+    else:
+        print(f"[bench] {w.name}: generating inputs", file=sys.stderr, flush=True)
+        q, k, v = (x.cuda() for x in workload_qkv(w))
     out = torch.empty_like(q)
     nb = w.n_blocks
     rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
@@ -237,23 +246,38 @@ def main():
 
     # Kept FLOP of every step s (host builder, outside the timed region).
     n_sweep = len(w.steps)
-    flops_of, nnz_of, host_us = {}, {}, []
+    flops_of, nnz_of = {}, {}
     for s in w.steps:
-        t0 = time.perf_counter()
         csr = L.build_mask(w.frames, w.tokens_per_frame, w.block, s, params)
-        host_us.append((time.perf_counter() - t0) * 1e6)
         hrp, hci = csr.arrays()
         flops_of[s] = kept_flops(hrp, hci, w.n_tokens, w.block, w.heads)
         nnz_of[s] = int(hrp[-1])
         csr.free()
+    # Host rebuild time (Sec. 2 quotes the metadata cost per denoising step):
+    # 20 rebuilds, cycling over the swept steps, after the ones above.
+    host_us = []
+    for i in range(20):
+        t0 = time.perf_counter()
+        L.build_mask(w.frames, w.tokens_per_frame, w.block, w.steps[i % n_sweep], params).free()
+        host_us.append((time.perf_counter() - t0) * 1e6)
     dense_flops = kept_flops(np.arange(nb + 1) * nb, np.tile(np.arange(nb), nb),
                              w.n_tokens, w.block, w.heads)
 
     if args.pmc:
-        m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, 10, rp, ci,
+        s_ref = 10 if 10 in w.steps else w.steps[0]
+        m = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
                                 params=params, stream=stream)
         for _ in range(3):
             L.attention(q, k, v, m, out=out, stream=stream)
+        ent = torch.empty(nb * nb, dtype=torch.int32, device="cuda")
+        rpx = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+        try:
+            me = L.build_exact_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rpx,
+                                           ent, params=params, stream=stream)
+            for _ in range(2):
+                L.attention_exact(q, k, v, me, out=out, stream=stream)
+        except L.LvsaError:
+            pass
         if not args.no_dense:
             L.dense_attention(q, k, v, block=w.block, out=out, stream=stream)
         src = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
@@ -390,19 +414,24 @@ def main():
     dense = {}
     if not args.no_dense:
         print("[bench] dense", file=sys.stderr, flush=True)
-        d_ms = median(time_calls(lambda: L.dense_attention(q, k, v, block=w.block,
-                                                           out=out, stream=stream), 5, 1))
-        # Dense attention also through the block-sparse kernel with a full
-        # mask (a window of T frames keeps every block), reported beside the
-        # dense entry point; the speedup divides by the dense entry point.
+        # Dense attention through the dense entry point, and through the
+        # block-sparse kernel with a full mask (a window of T frames keeps
+        # every block), timed in alternation (two calls of each, three
+        # times) so that the board's clock drift weighs on both alike; the
+        # speedup divides by the dense entry point.
         full = L.Params(budget_frames=w.budget_frames, window=w.frames, tper=w.frames,
                         text_tokens=w.text_tokens)
         mf = L.build_mask_device(w.frames, w.tokens_per_frame, w.block, s_ref, rp, ci,
                                  params=full, stream=stream)
         torch.cuda.synchronize()
         assert int(rp[-1]) == nb * nb, "full mask expected"
-        f_ms = median(time_calls(lambda: L.attention(q, k, v, mf, out=out, stream=stream),
-                                 5, 1))
+        d_all, f_all = [], []
+        for rnd in range(3):
+            d_all += time_calls(lambda: L.dense_attention(q, k, v, block=w.block, out=out,
+                                                          stream=stream), 2, 1 if rnd == 0 else 0)
+            f_all += time_calls(lambda: L.attention(q, k, v, mf, out=out, stream=stream),
+                                2, 1 if rnd == 0 else 0)
+        d_ms, f_ms = median(d_all), median(f_all)
         dense = {
             "dense_ms_per_call": d_ms,
             "dense_full_mask_ms_per_call": f_ms,

@@ -673,6 +673,15 @@ __device__ __forceinline__ void attn_tile(
       w2 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(2, n - 1)]);
     }
   } else {
+    // Dense: the words nb-1 .. 0 (both query blocks keep every key block),
+    // written to LDS and read from there like the merged walk's (timed
+    // faster than computing them in the loop: 1.7% at the Wan-1.3B 6x shape
+    // and 2.9% at 40 heads, interleaved on one board); steps past WALK_CAP
+    // compute theirs.
+    __syncthreads();
+    for (int t = threadIdx.x; t < min(nb, WALK_CAP); t += TL::NT)
+      walk.w[t] = (uint32_t)(nb - 1 - t) | 0xC0000000u;
+    __syncthreads();
     w0 = (uint32_t)(nb - 1) | 0xC0000000u;
     w1 = (uint32_t)max(nb - 2, 0) | 0xC0000000u;
     w2 = (uint32_t)max(nb - 3, 0) | 0xC0000000u;
@@ -722,9 +731,10 @@ __device__ __forceinline__ void attn_tile(
     __syncthreads();
     for (int j = 0; j < n; ++j) {
       // Word of step j+3 from the walk's LDS, read now and used at the end of
-      // the step (the last word again past the end of the walk).
-      uint32_t w3v = 0u;
-      if constexpr (SPARSE) w3v = walk.w[min(j + 3, n - 1)];
+      // the step (the last word again past the end of the walk; a sparse
+      // walk never passes WALK_CAP words, nb <= WALK_CAP).
+      const int g3 = min(j + 3, n - 1);
+      const uint32_t w3v = walk.w[min(g3, WALK_CAP - 1)];
       const StepLoads<BLOCK> sl{
           (uint32_t)__builtin_amdgcn_readfirstlane(k_slot0 + (uint32_t)(j & 1) * TL::BYTES),
           (uint32_t)__builtin_amdgcn_readfirstlane(v_slot0 + (uint32_t)((j + 1) & 1) * TL::BYTES),
@@ -748,8 +758,8 @@ __device__ __forceinline__ void attn_tile(
       }
       wait_loads_and_sync();
       w1 = w2;
-      w2 = SPARSE ? (uint32_t)__builtin_amdgcn_readfirstlane((int)w3v)
-                  : (uint32_t)max(nb - 4 - j, 0) | 0xC0000000u;
+      w2 = SPARSE || g3 < WALK_CAP ? (uint32_t)__builtin_amdgcn_readfirstlane((int)w3v)
+                                   : (uint32_t)(nb - 1 - g3) | 0xC0000000u;
     }
     __syncthreads();
   }

@@ -275,6 +275,13 @@ def test_attention_rejects_before_launch():
         (dict(m=L.BlockMask(1000, 128, nb, nb, 0, 0x3000)), L.EINVAL),
         (dict(m=L.BlockMask(1000, 128, nb, nb, 0x2000, 0)), L.EINVAL),
     ]
+    # sparse launches merge a pair's two CSR rows in LDS: nb <= 8000
+    big_n = 8001 * 128
+    big = [_t(a, heads=1, n=big_n) for a in (0x10000, 0x20000, 0x30000, 0x40000)]
+    st = lib.lvsa_attention(ref(big[0]), ref(big[1]), ref(big[2]),
+                            ref(L.BlockMask(big_n, 128, 8001, 8001, 0x2000, 0x3000)),
+                            ref(big[3]), None)
+    assert st == L.EUNSUPPORTED
     for over, want in cases:
         a = dict(q=q, k=k, v=v, o=o, m=m)
         a.update(over)

@@ -410,3 +410,21 @@ def test_shared_mask_on_two_streams(T, P, B, H):
         fref = OA.frame_sparse_attention(qq, kf, vf, A, P)
         err = np.abs(oe.float().cpu().numpy() - fref)
         assert_close(float(err.max()), float(err.mean()))
+
+
+def test_dense_past_the_lds_word_array():
+    """Dense attention with more key blocks than the walk's LDS word array
+    (nb = 8100 > 8000 at B = 64): every tile's last steps take computed
+    words; sampled rows against Eq. 1."""
+    B, H = 64, 1
+    nb = 8100
+    N = nb * B - 37                     # ragged last block
+    _say(f"[dense-long] N={N} B={B} nb={nb}")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(8100)
+    q, k, v = (torch.randn((H, N, 128), generator=g).to(torch.bfloat16) for _ in range(3))
+    out = L.dense_attention(q.cuda(), k.cuda(), v.cuda(), block=B)
+    torch.cuda.synchronize()
+    rp = [i * nb for i in range(nb + 1)]
+    ci = list(range(nb)) * nb
+    assert_close(*compare_rows(out, q, k, v, rp, ci, B, [0], [0, 4000, nb - 1]))
