@@ -389,10 +389,13 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
     for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
 }
 
-// GEMM phase of the ping-pong schedule: O += P(j) V(j) and l += the row sums
-// of P(j) (one 16x16x32 MFMA per 16-key step, `ones` its A operand), then
+// GEMM phase of the ping-pong schedule: l += the row sums of P(j) (one
+// 16x16x32 MFMA per 16-key step, `ones` its A operand), O += P(j) V(j), then
 // S(j+1) = K(j+1) Q^T into `sc`, with K and V fragments read AHEAD MFMAs
-// early and the tile loads in `sl` (may be null) spread over the phase.
+// early and the tile loads in `sl` (may be null) spread over the phase.  The
+// row-sum MFMAs come first: their operands are already in registers, so they
+// run while the first fragments arrive from LDS (0.2-1.2% faster than
+// after P V, interleaved on one board).
 template <int BLOCK>
 __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
                                            const bf16x8 (&qf)[8], Scores<BLOCK>& sc,
@@ -428,18 +431,19 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
   for (int i = 0; i < AHEAD; ++i) fr[i] = frag(i);
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
+  for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      st.l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[kt2][c2], st.l, 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
   for (int i = 0; i < NF; ++i) {
     if (i + AHEAD < NF) fr[i + AHEAD] = frag(i + AHEAD);
     if (sl && i % (NF / NLOADS) == 0) issue_step_load<BLOCK>(*sl, i / (NF / NLOADS));
     if (i < NP) {
       const int dt = i / (2 * TL::KTW), kt = (i / 2) % TL::KTW, c = i % 2;
       st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i], pr.p[kt][c], st.o[dt], 0, 0, 0);
-      if (i == NP - 1)
-#pragma unroll
-        for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2)
-            st.l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[kt2][c2], st.l, 0, 0, 0);
     } else {
       const int f = i - NP;
       const int kt = f / 8, stp = f % 8;
