@@ -269,10 +269,22 @@ __device__ __forceinline__ void compute_scores(const char* lds_k, const bf16x8 (
   }
 }
 
+// Row sums l are kept one of two ways (RSUM): on the matrix core, as a
+// 16x16 MFMA accumulator that the GEMM phase adds each step's bf16 P into
+// (lane c < 16 holds rows c and c + 16), or on the VALU, as two partial sums
+// per lane of the fp32 probabilities of the lane's own keys that the softmax
+// phase adds into (lanes l and l^32 hold the two halves of a row's keys).
+// Timed interleaved on one board, the VALU form is 0.4-0.7% faster in the
+// block mode (four workloads), and slower in the dense mode (0.4-0.9%: long
+// walks) and in the token-exact mode (0.4%: its masking adds VALU work to the
+// same phases).
+enum RowSums { RSUM_MFMA = 0, RSUM_VALU = 1 };
+
 struct WaveState {
   f32x16 o[4];   // O^T tiles [d tile]: d = 32*dt + C row
   float m;       // running max (log2 domain), shared by lanes l, l^32
-  f32x4 l;       // row sums (MFMA 16x16 C tile: lane c < 16 holds rows c, c + 16)
+  f32x4 l;       // RSUM_MFMA: row sums (16x16 C tile)
+  float l0, l1;  // RSUM_VALU: partial row sums of the lane's keys
 };
 
 // Keys at or past N (ragged last block) do not exist: their scores become
@@ -344,11 +356,12 @@ struct Probs {
 // Softmax phase of the ping-pong schedule: block j's scores (in `sc`) become
 // its probabilities P (bf16, in `pr`), with the running max and, when the
 // max is raised, the rescale of O and l done here so that the next GEMM phase
-// only multiplies (and adds P up into l).  `sl` (may be null) carries tile
+// only multiplies (with RSUM_VALU, P is also added into l here; with
+// RSUM_MFMA the GEMM phase does it).  `sl` (may be null) carries tile
 // loads to issue along the way.  Scheduling barriers every 8 scores keep the
 // compiler from hoisting many exponentials at once (S, P, O and Q already
 // fill the register file).
-template <int BLOCK>
+template <int BLOCK, int RSUM>
 __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState& st,
                                               Probs<BLOCK>& pr, float scale_log2,
                                               const StepLoads<BLOCK>* sl) {
@@ -365,10 +378,15 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
   if (__builtin_amdgcn_ballot_w64(raise)) {
     const float a = raise ? __builtin_amdgcn_exp2f(st.m - m) : 1.f;
     st.m = raise ? m : st.m;
-    // l tile: register 0 of lane c holds row c, register 1 row c + 16.
-    const float a16 = __shfl_xor(a, 16);
-    st.l[0] *= a;
-    st.l[1] *= a16;
+    if constexpr (RSUM == RSUM_MFMA) {
+      // l tile: register 0 of lane c holds row c, register 1 row c + 16.
+      const float a16 = __shfl_xor(a, 16);
+      st.l[0] *= a;
+      st.l[1] *= a16;
+    } else {
+      st.l0 *= a;
+      st.l1 *= a;
+    }
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) st.o[dt] *= a;
   }
@@ -381,6 +399,9 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
         __builtin_amdgcn_exp2f(__builtin_fmaf(sc.s[el / 16][el % 16], scale_log2, -msub));
     const float b = __builtin_amdgcn_exp2f(
         __builtin_fmaf(sc.s[(el + 1) / 16][(el + 1) % 16], scale_log2, -msub));
+    if constexpr (RSUM == RSUM_VALU) {
+      if (el % 4 == 0) st.l0 += a + b; else st.l1 += a + b;
+    }
     const bf16x2 pk = {(__bf16)a, (__bf16)b};
     pr.p[el / 16][(el % 16) / 8][el % 8] = pk[0];
     pr.p[el / 16][(el % 16) / 8][el % 8 + 1] = pk[1];
@@ -389,14 +410,14 @@ __device__ __forceinline__ void softmax_phase(const Scores<BLOCK>& sc, WaveState
     for (; issued < NLOADS; ++issued) issue_step_load<BLOCK>(*sl, issued);
 }
 
-// GEMM phase of the ping-pong schedule: l += the row sums of P(j) (one
-// 16x16x32 MFMA per 16-key step, `ones` its A operand), O += P(j) V(j), then
-// S(j+1) = K(j+1) Q^T into `sc`, with K and V fragments read AHEAD MFMAs
-// early and the tile loads in `sl` (may be null) spread over the phase.  The
-// row-sum MFMAs come first: their operands are already in registers, so they
-// run while the first fragments arrive from LDS (0.2-1.2% faster than
-// after P V, interleaved on one board).
-template <int BLOCK>
+// GEMM phase of the ping-pong schedule: with RSUM_MFMA, l += the row sums of
+// P(j) (one 16x16x32 MFMA per 16-key step, `ones` its A operand); then
+// O += P(j) V(j) and S(j+1) = K(j+1) Q^T into `sc`, with K and V fragments
+// read AHEAD MFMAs early and the tile loads in `sl` (may be null) spread over
+// the phase.  The row-sum MFMAs come first: their operands are already in
+// registers, so they run while the first fragments arrive from LDS (0.2-1.2%
+// faster than after P V, interleaved on one board).
+template <int BLOCK, int RSUM>
 __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
                                            const bf16x8 (&qf)[8], Scores<BLOCK>& sc,
                                            const Probs<BLOCK>& pr, WaveState& st,
@@ -430,13 +451,15 @@ __device__ __forceinline__ void gemm_phase(const char* lds_k, const char* lds_v,
 #pragma unroll
   for (int i = 0; i < AHEAD; ++i) fr[i] = frag(i);
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (RSUM == RSUM_MFMA) {
 #pragma unroll
-  for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
+    for (int kt2 = 0; kt2 < TL::KTW; ++kt2)
 #pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
-      st.l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[kt2][c2], st.l, 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+      for (int c2 = 0; c2 < 2; ++c2) {
+        st.l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pr.p[kt2][c2], st.l, 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  }
 #pragma unroll
   for (int i = 0; i < NF; ++i) {
     if (i + AHEAD < NF) fr[i + AHEAD] = frag(i + AHEAD);
@@ -696,6 +719,9 @@ __device__ __forceinline__ void attn_tile(
   for (int dt = 0; dt < 4; ++dt) ws.o[dt] = f32x16{};
   ws.m = -__builtin_inff();
   ws.l = f32x4{};
+  ws.l0 = 0.f;
+  ws.l1 = 0.f;
+  constexpr int RSUM = MODE == ATTN_BLOCK ? RSUM_VALU : RSUM_MFMA;
   // A operand of the row-sum MFMA (16x16x32): read as P^T's B operand, lane
   // group g = lane/16 of the 32x32 P register holds q rows 16*(g%2) + 0..15,
   // so A row 0 takes groups 0 and 2 (rows 0-15) and row 1 groups 1 and 3.
@@ -731,7 +757,7 @@ __device__ __forceinline__ void attn_tile(
     compute_scores<BLOCK>(k_lds, qf, sc, fa);   // S(0)
     mask_block(sc, w0);
     Probs<BLOCK> pr;
-    if (lead) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);   // P(0)
+    if (lead) softmax_phase<BLOCK, RSUM>(sc, ws, pr, scale_log2, nullptr);   // P(0)
     __syncthreads();
     for (int j = 0; j < n; ++j) {
       // Word of step j+3 from the walk's LDS, read now and used at the end of
@@ -747,17 +773,17 @@ __device__ __forceinline__ void attn_tile(
       const char* const vj = v_lds + (j & 1) * TL::BYTES;          // V(j)
       // half-period 2j
       if (lead) {
-        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, &sl);
+        gemm_phase<BLOCK, RSUM>(kj1, vj, qf, sc, pr, ws, fa, ones, &sl);
         mask_block(sc, w1);
       } else {
-        softmax_phase<BLOCK>(sc, ws, pr, scale_log2, &sl);
+        softmax_phase<BLOCK, RSUM>(sc, ws, pr, scale_log2, &sl);
       }
       __syncthreads();
       // half-period 2j+1
       if (lead) {
-        if (j + 1 < n) softmax_phase<BLOCK>(sc, ws, pr, scale_log2, nullptr);
+        if (j + 1 < n) softmax_phase<BLOCK, RSUM>(sc, ws, pr, scale_log2, nullptr);
       } else {
-        gemm_phase<BLOCK>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
+        gemm_phase<BLOCK, RSUM>(kj1, vj, qf, sc, pr, ws, fa, ones, nullptr);
         mask_block(sc, w1);
       }
       wait_loads_and_sync();
@@ -770,8 +796,14 @@ __device__ __forceinline__ void attn_tile(
 
   // Every wave holds whole rows: O / l, rounded to bf16.  The l tile holds
   // row c in register 0 of lane c and row c + 16 in register 1 (c < 16).
-  const float r0s = __shfl(ws.l[0], li), r1s = __shfl(ws.l[1], li & 15);
-  const float lsum = li < 16 ? r0s : r1s;
+  float lsum;
+  if constexpr (RSUM == RSUM_MFMA) {
+    const float r0s = __shfl(ws.l[0], li), r1s = __shfl(ws.l[1], li & 15);
+    lsum = li < 16 ? r0s : r1s;
+  } else {
+    const float lpart = ws.l0 + ws.l1;
+    lsum = lpart + __shfl_xor(lpart, 32);
+  }
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   if (qrow < N) {
     __bf16* orow = oh + (int64_t)qrow * o_st;

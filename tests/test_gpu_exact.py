@@ -62,8 +62,12 @@ def test_exact_full_output_matches_eq2(T, P, B, H, W, tper):
 
 
 def test_exact_equals_block_mode_when_block_divides_frame():
-    """P mod B = 0: every kept block is whole, so the two forms are the same
-    computation and give the same bits."""
+    """P mod B = 0: every kept block is whole, so the two forms attend the
+    same keys with the same scores and probabilities.  They keep the row sums
+    differently (fp32 adds of the probabilities in the block form, matrix-core
+    sums of their bf16 values in the token-exact form), which moves the
+    normalised output by far less than half a bf16 unit: the two agree to one
+    unit in the last place of bf16."""
     w = WORKLOADS["tiny"]
     q, k, v = (x.cuda() for x in workload_qkv(w))
     for step in w.steps:
@@ -74,7 +78,9 @@ def test_exact_equals_block_mode_when_block_divides_frame():
         a = L.attention(q, k, v, csr.device_mask())
         b = L.attention_exact(q, k, v, csr.exact_mask())
         torch.cuda.synchronize()
-        assert torch.equal(a, b)
+        af, bf = a.float(), b.float()
+        assert bool(((af - bf).abs() <= af.abs() * 2.0 ** -7 + 1e-7).all())
+        assert float((af - bf).abs().mean()) < 1e-5
 
 
 def _sample_rows(w, csr_rp, n_random=6, seed=1):
