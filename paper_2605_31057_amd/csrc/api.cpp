@@ -238,6 +238,42 @@ lvsa_status upload_array(const std::vector<T>& host, T** dev, hipStream_t s) {
   return LVSA_OK;
 }
 
+// Host arrays of freed handles, handed to the next builds: a denoising loop
+// frees step s's mask and builds step s+1's of the same shape, and reusing
+// the arrays' memory skips the page faults of fresh allocations (most of a
+// rebuild's cost).  At most kHostPool sets are kept.
+struct HostArrays {
+  std::vector<int32_t> row_ptr, col_idx;
+  std::vector<uint32_t> entry;
+};
+constexpr size_t kHostPool = 4;
+std::mutex g_host_pool_mu;
+std::vector<HostArrays> g_host_pool;
+
+void take_host_arrays(lvsa_csr* h) {
+  std::lock_guard<std::mutex> lock(g_host_pool_mu);
+  if (g_host_pool.empty()) return;
+  HostArrays& a = g_host_pool.back();
+  h->row_ptr.swap(a.row_ptr);
+  h->col_idx.swap(a.col_idx);
+  h->entry.swap(a.entry);
+  g_host_pool.pop_back();
+}
+
+void give_host_arrays(lvsa_csr* h) {
+  std::lock_guard<std::mutex> lock(g_host_pool_mu);
+  if (g_host_pool.size() >= kHostPool) return;
+  try {
+    g_host_pool.emplace_back();
+  } catch (const std::bad_alloc&) {
+    return;
+  }
+  HostArrays& a = g_host_pool.back();
+  a.row_ptr.swap(h->row_ptr);
+  a.col_idx.swap(h->col_idx);
+  a.entry.swap(h->entry);
+}
+
 }  // namespace
 
 using namespace lvsa;
@@ -327,6 +363,8 @@ lvsa_status build_mask_handle(int32_t T, int32_t P, int32_t B, int32_t step,
   lvsa_csr* h = new (std::nothrow) lvsa_csr();
   if (!h) return LVSA_ENOMEM;
   h->has_entry = exact;
+  take_host_arrays(h);
+  if (!exact) h->entry.clear();
   try {
     build_csr_host(c, P, B, &h->row_ptr, &h->col_idx, h->has_entry ? &h->entry : nullptr);
   } catch (const std::bad_alloc&) {
@@ -404,6 +442,7 @@ void lvsa_csr_free(lvsa_csr* csr) {
   for (void* d : {(void*)csr->d_row_ptr, (void*)csr->d_col_idx, (void*)csr->d_entry})
     if (d) (void)hipFreeAsync(d, csr->upload_stream);
   if (csr->uploaded) (void)hipEventDestroy(csr->uploaded);
+  give_host_arrays(csr);
   delete csr;
 }
 

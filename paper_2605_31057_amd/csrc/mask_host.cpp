@@ -19,6 +19,12 @@
 //
 // The token-exact entry words (lvsa.h) are built alongside when asked for:
 // one word per kept block, from the two (at most) frames of each side.
+//
+// A rebuild runs once per denoising step, so its cost is mostly that of
+// touching fresh memory: the working arrays are per-thread and kept between
+// calls, and the output arrays come from the handles the caller has freed
+// (api.cpp), so a loop that frees step s's mask before building step s+1's
+// allocates nothing after the first step.
 #include <algorithm>
 #include <cstring>
 
@@ -34,8 +40,11 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
   const int32_t S = c.text > 0 ? T + 1 : T;   // segments: frames, then text
-  std::vector<int32_t> lo(T), hi(T);
-  std::vector<uint8_t> anchor(T);
+  thread_local std::vector<int32_t> lo, hi;
+  thread_local std::vector<uint8_t> anchor;
+  lo.resize(T);
+  hi.resize(T);
+  anchor.resize(T);
   for (int32_t t = 0; t < T; ++t) {
     anchor[t] = is_anchor(c, t) ? 1 : 0;
     frame_window(c, t, &lo[t], &hi[t]);
@@ -45,8 +54,8 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
   };
   // Per key block: its frames and split point, so an entry word costs four
   // table lookups.
-  std::vector<int32_t> kg0, kg1;
-  std::vector<uint32_t> kfirst;
+  thread_local std::vector<int32_t> kg0, kg1;
+  thread_local std::vector<uint32_t> kfirst;
   if (entry) {
     kg0.resize(nb);
     kg1.resize(nb);
@@ -57,11 +66,15 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
 
   // Pass 1: the distinct rows (one per run of query blocks touching the same
   // frames) into small scratch arrays, and every row's length.
-  std::vector<int32_t> uniq;
-  std::vector<uint32_t> uniq_e;
-  std::vector<int64_t> src(nb);
+  thread_local std::vector<int32_t> uniq;
+  thread_local std::vector<uint32_t> uniq_e;
+  thread_local std::vector<int64_t> src;
+  thread_local std::vector<uint8_t> attended;
+  uniq.clear();
+  uniq_e.clear();
+  src.resize(nb);
+  attended.resize(S);
   row_ptr->assign(nb + 1, 0);
-  std::vector<uint8_t> attended(S);
   int32_t prev_first = -1, prev_last = -1;
   int64_t prev_begin = 0, prev_len = 0;
   for (int32_t qb = 0; qb < nb; ++qb) {
@@ -82,10 +95,16 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
         if (!attended[tau]) continue;
         int32_t b0, b1;
         segment_blocks(tau, T, P, B, N, &b0, &b1);
-        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b) {
-          uniq.push_back(b);
-          if (entry)
-            uniq_e.push_back(exact_word(b, kg0[b], kg1[b], kfirst[b], f0, f1, attends));
+        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b) uniq.push_back(b);
+        if (entry) {
+          // A block inside segment tau has the same word as its neighbours
+          // but for kb: the 2x2 pattern collapses to tau's two rows.
+          const uint32_t q0 = attends(f0, tau) ? 3u : 0u, q1 = attends(f1, tau) ? 12u : 0u;
+          const uint32_t inner = ((uint32_t)B << 16) | ((q0 | q1) << 24);
+          for (int32_t b = std::max(b0, last + 1); b <= b1; ++b)
+            uniq_e.push_back(kg0[b] == kg1[b]
+                                 ? (uint32_t)b | inner
+                                 : exact_word(b, kg0[b], kg1[b], kfirst[b], f0, f1, attends));
         }
         last = std::max(last, b1);
       }

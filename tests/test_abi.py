@@ -445,6 +445,35 @@ def test_host_builder_with_text_matches_oracle(T, P, B, Lt):
             assert all(np.array_equal(x, y) for x, y in zip(blk.arrays(), (row_ptr, col_idx)))
 
 
+def test_rebuilds_after_free_match_the_oracle():
+    """Freed handles hand their host arrays to later builds: a sequence of
+    builds of different sizes and forms, each freed before the next, gives
+    every mask bit for bit as a fresh oracle build does (no stale entries from
+    a larger earlier mask, no entry words left on a block-only handle)."""
+    seq = [  # T, P, B, Lt, exact
+        (9, 150, 64, 0, True), (4, 70, 64, 0, False), (12, 96, 64, 40, True),
+        (5, 200, 128, 0, False), (5, 200, 128, 0, True), (3, 255, 128, 7, True),
+        (9, 150, 64, 0, False),
+    ]
+    for rep in range(2):
+        for i, (T, P, B, Lt, exact) in enumerate(seq):
+            s = i + rep
+            p = L.Params(budget_frames=0, window=1, tper=3, text_tokens=Lt)
+            csr = L.build_mask(T, P, B, s, p, exact=exact)
+            row_ptr, col_idx = csr.arrays()
+            want_rp, want_ci = M.build_mask(T, P, B, s, W=1, tper=3, text=Lt)
+            assert row_ptr.tolist() == want_rp and col_idx.tolist() == want_ci, (rep, i)
+            if exact:
+                _, _, A = M.attended_frames(T, s, W=1, tper=3)
+                got = decode_entries(row_ptr, col_idx, csr.entries(), T, P, B, Lt)
+                want = M.token_mask_text(A, T, P, Lt) if Lt else M.token_mask(A, T, P)
+                assert np.array_equal(got, want), (rep, i)
+            else:
+                with pytest.raises(L.LvsaError):
+                    csr.entries()
+            csr.free()
+
+
 def test_host_builder_text_on_hv_horizon():
     """HunyuanVideo 1.5 at 2x (65 x 30x53, C = 33) with 512 text tokens."""
     T, P, B, Lt = 65, 1590, 128, 512
