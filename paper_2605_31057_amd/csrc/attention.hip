@@ -688,23 +688,14 @@ __device__ __forceinline__ void attn_tile(
   // that no later step reads.
   int n = nb;
   uint32_t w0 = 0u, w1 = 0u, w2 = 0u;
-  if constexpr (SPARSE) {
-    const int32_t r0 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq]);
-    const int32_t r1 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 1]);
-    const int32_t r2 =
-        2 * pq + 1 < nb ? __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 2]) : r1;
-    n = merge_pair<TL::NT, EXACT>(walk, (uint32_t*)lds, rows, r0, r1, r1, r2, nb);
-    if (n > 0) {
-      w0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[0]);
-      w1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(1, n - 1)]);
-      w2 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(2, n - 1)]);
-    }
-  } else {
-    // Dense: the words nb-1 .. 0 (both query blocks keep every key block),
-    // written to LDS and read from there like the merged walk's (timed
-    // faster than computing them in the loop: 1.7% at the Wan-1.3B 6x shape
-    // and 2.9% at 40 heads, interleaved on one board); steps past WALK_CAP
-    // compute theirs.
+  // Dense: the words nb-1 .. 0 (both query blocks keep every key block),
+  // written to LDS and read from there like the merged walk's (timed faster
+  // than computing them in the loop: 1.7% at the Wan-1.3B 6x shape and 2.9%
+  // at 40 heads, interleaved on one board); steps past WALK_CAP compute
+  // theirs.  The block mode runs dense attention this way when it is given
+  // no CSR (row_ptr null, nb <= WALK_CAP): the same code as a full mask's
+  // walk, without the merge.
+  auto dense_words = [&]() {
     __syncthreads();
     for (int t = threadIdx.x; t < min(nb, WALK_CAP); t += TL::NT)
       walk.w[t] = (uint32_t)(nb - 1 - t) | 0xC0000000u;
@@ -712,6 +703,24 @@ __device__ __forceinline__ void attn_tile(
     w0 = (uint32_t)(nb - 1) | 0xC0000000u;
     w1 = (uint32_t)max(nb - 2, 0) | 0xC0000000u;
     w2 = (uint32_t)max(nb - 3, 0) | 0xC0000000u;
+  };
+  if constexpr (SPARSE) {
+    if (EXACT || row_ptr != nullptr) {
+      const int32_t r0 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq]);
+      const int32_t r1 = __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 1]);
+      const int32_t r2 =
+          2 * pq + 1 < nb ? __builtin_amdgcn_readfirstlane(row_ptr[2 * pq + 2]) : r1;
+      n = merge_pair<TL::NT, EXACT>(walk, (uint32_t*)lds, rows, r0, r1, r1, r2, nb);
+      if (n > 0) {
+        w0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[0]);
+        w1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(1, n - 1)]);
+        w2 = (uint32_t)__builtin_amdgcn_readfirstlane((int)walk.w[min(2, n - 1)]);
+      }
+    } else {
+      dense_words();
+    }
+  } else {
+    dense_words();
   }
 
   WaveState ws;
@@ -957,6 +966,18 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t stream) {
 
 hipError_t launch_attention(const AttnArgs& a, int32_t block, AttnMode mode,
                             hipStream_t stream) {
+  // Dense attention over at most WALK_CAP key blocks runs the block mode's
+  // kernel without a CSR: the same code as the block-sparse kernel with a
+  // full mask, which it matched or beat only that way (the separate dense
+  // instantiation timed 0.6% slower than the full-mask launch at the
+  // Wan-1.3B 6x shape, interleaved on one board, for no difference in its
+  // step loop but the layout of its branches).
+  if (mode == ATTN_DENSE && a.n_blocks <= WALK_CAP) {
+    AttnArgs d = a;
+    d.row_ptr = nullptr;
+    d.rows = nullptr;
+    return launch_attention(d, block, ATTN_BLOCK, stream);
+  }
   if (block == 128) {
     if (mode == ATTN_EXACT) return launch_t<128, ATTN_EXACT>(a, stream);
     if (mode == ATTN_BLOCK) return launch_t<128, ATTN_BLOCK>(a, stream);
