@@ -416,7 +416,7 @@ def main():
         print("[bench] dense", file=sys.stderr, flush=True)
         # Dense attention through the dense entry point, and through the
         # block-sparse kernel with a full mask (a window of T frames keeps
-        # every block), timed in alternation (two calls of each, three
+        # every block), timed in alternation (two calls of each, five
         # times) so that the board's clock drift weighs on both alike; the
         # speedup divides by the dense entry point.
         full = L.Params(budget_frames=w.budget_frames, window=w.frames, tper=w.frames,
@@ -426,7 +426,7 @@ def main():
         torch.cuda.synchronize()
         assert int(rp[-1]) == nb * nb, "full mask expected"
         d_all, f_all = [], []
-        for rnd in range(3):
+        for rnd in range(5):
             d_all += time_calls(lambda: L.dense_attention(q, k, v, block=w.block, out=out,
                                                           stream=stream), 2, 1 if rnd == 0 else 0)
             f_all += time_calls(lambda: L.attention(q, k, v, mf, out=out, stream=stream),
