@@ -334,6 +334,36 @@ def test_random_csr_one_block_rows_and_full_rows():
     assert_close(float(err.max()), float(err.mean()))
 
 
+def test_csr_at_the_block_limit():
+    """nb = 8000 key blocks (B = 64), the most the sparse kernels take: rows 0
+    and 1 keep every block (their merged walk fills the 8000-word LDS array
+    over 16 merge passes), the last pair keeps different blocks in each row,
+    the others keep the diagonal and two random blocks; sampled query blocks
+    against the oracle."""
+    B, H, nb = 64, 1, 8000
+    N = nb * B - 19                     # ragged last block
+    rng = np.random.default_rng(8000)
+    rp, ci = [0], []
+    for r in range(nb):
+        if r < 2:
+            cols = list(range(nb))
+        elif r >= nb - 2:
+            cols = sorted({r, int(rng.integers(0, nb)), (r * 37) % nb, 5 * (r % 2)})
+        else:
+            cols = sorted({r, int(rng.integers(0, nb)), int(rng.integers(0, nb))})
+        ci.extend(cols)
+        rp.append(len(ci))
+    _say(f"[csr-limit] N={N} B={B} nb={nb} nnz={len(ci)}")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(80)
+    q, k, v = (torch.randn((H, N, 128), generator=g).to(torch.bfloat16) for _ in range(3))
+    m = L.csr_mask(torch.tensor(rp, dtype=torch.int32, device="cuda"),
+                   torch.tensor(ci, dtype=torch.int32, device="cuda"), N, B)
+    out = L.attention(q.cuda(), k.cuda(), v.cuda(), m)
+    torch.cuda.synchronize()
+    assert_close(*compare_rows(out, q, k, v, rp, ci, B, [0], [0, 1, 2, 4001, nb - 2, nb - 1]))
+
+
 def test_empty_rows_give_zeros():
     """A query block whose CSR row is empty gets zeros; its pair partner is
     unaffected."""
@@ -412,16 +442,17 @@ def test_shared_mask_on_two_streams(T, P, B, H):
         assert_close(float(err.max()), float(err.mean()))
 
 
-def test_dense_past_the_lds_word_array():
-    """Dense attention with more key blocks than the walk's LDS word array
-    (nb = 8100 > 8000 at B = 64): every tile's last steps take computed
-    words; sampled rows against Eq. 1."""
+@pytest.mark.parametrize("nb", [8000, 8100])
+def test_dense_at_and_past_the_lds_word_array(nb):
+    """Dense attention at the walk's LDS word array capacity (nb = 8000 at
+    B = 64: the block-mode kernel without a CSR, every word in LDS) and past
+    it (nb = 8100: the dense kernel, whose tiles' last steps take computed
+    words); sampled rows against Eq. 1."""
     B, H = 64, 1
-    nb = 8100
     N = nb * B - 37                     # ragged last block
     _say(f"[dense-long] N={N} B={B} nb={nb}")
     g = torch.Generator(device="cpu")
-    g.manual_seed(8100)
+    g.manual_seed(nb)
     q, k, v = (torch.randn((H, N, 128), generator=g).to(torch.bfloat16) for _ in range(3))
     out = L.dense_attention(q.cuda(), k.cuda(), v.cuda(), block=B)
     torch.cuda.synchronize()
