@@ -353,7 +353,10 @@ lvsa_status lvsa_attention_exact(const lvsa_tensor* q, const lvsa_tensor* k,
                                  void* stream);
 
 /* Dense attention forward (Eq. 1 over all N keys), the same kernel design
- * visiting every key block; `block` (64 or 128) is its tile size.
+ * visiting every key block; `block` (64 or 128) is its tile size.  Up to
+ * 8000 key blocks it runs the block-sparse kernel with every block kept (no
+ * CSR is read or allocated); past that, a dense instantiation of the same
+ * kernel.  No upper limit on N beyond the tensor checks.
  * Errors as for lvsa_attention. */
 lvsa_status lvsa_dense_attention(const lvsa_tensor* q, const lvsa_tensor* k,
                                  const lvsa_tensor* v, int32_t block,
