@@ -145,6 +145,10 @@ lvsa_status lvsa_frame_window(int32_t T, int32_t step, const lvsa_params* p,
 typedef struct lvsa_csr lvsa_csr; /* opaque, library-owned */
 
 /* Host builder (the paper builds this metadata on the CPU once per step).
+ * Thread-safe and reentrant: each calling thread keeps its own working
+ * arrays between calls, and lvsa_csr_free passes a handle's host arrays on
+ * to later builds (at most 4 sets kept, behind a lock), so a loop that frees
+ * step s's handle before building step s+1's touches no fresh memory.
  *   T >= 1 frames (<= LVSA_MAX_FRAMES), P >= 1 tokens per frame,
  *   1 <= B <= 2^20 tokens per block (the attention kernels take 64 or 128),
  *   T*P + B < 2^31 and nb*nb < 2^31 (so nnz fits int32), step >= 0,

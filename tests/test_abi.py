@@ -474,6 +474,36 @@ def test_rebuilds_after_free_match_the_oracle():
             csr.free()
 
 
+def test_host_builds_from_threads_match_the_oracle():
+    """Builds and frees from four threads at once (ctypes releases the GIL
+    around each call) give the oracle's masks: the per-thread working arrays
+    and the shared pool of freed arrays do not mix masks."""
+    import threading
+    cases = [(9, 150, 64, 0), (12, 96, 64, 40), (5, 200, 128, 0), (7, 100, 64, 0)]
+    want = {c: M.build_mask(c[0], c[1], c[2], 2, W=1, tper=3, text=c[3]) for c in cases}
+    errors = []
+
+    def work(i):
+        try:
+            for rep in range(30):
+                T, P, B, Lt = cases[(i + rep) % len(cases)]
+                p = L.Params(budget_frames=0, window=1, tper=3, text_tokens=Lt)
+                csr = L.build_mask(T, P, B, 2, p, exact=rep % 2 == 0)
+                rp, ci = csr.arrays()
+                if (rp.tolist(), ci.tolist()) != tuple(want[(T, P, B, Lt)]):
+                    errors.append((i, rep))
+                csr.free()
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors[:5]
+
+
 def test_host_builder_text_on_hv_horizon():
     """HunyuanVideo 1.5 at 2x (65 x 30x53, C = 33) with 512 text tokens."""
     T, P, B, Lt = 65, 1590, 128, 512
