@@ -32,6 +32,29 @@
 
 namespace lvsa {
 
+namespace {
+
+// Working arrays of one thread's builds, kept between calls.
+struct HostScratch {
+  std::vector<int32_t> lo, hi, kg0, kg1, uniq;
+  std::vector<uint32_t> kfirst, uniq_e;
+  std::vector<int64_t> src;
+  std::vector<uint8_t> anchor, attended;
+};
+
+HostScratch& host_scratch() {
+  thread_local HostScratch s;
+  return s;
+}
+
+// Room for `more` values past `used` (grown geometrically, so rarely).
+template <typename V>
+void ensure(std::vector<V>& v, size_t used, size_t more) {
+  if (used + more > v.size()) v.resize(std::max(2 * v.size(), used + more));
+}
+
+}  // namespace
+
 void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
                     std::vector<int32_t>* row_ptr,
                     std::vector<int32_t>* col_idx,
@@ -40,11 +63,13 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
   const int32_t N = (int32_t)mask_tokens(c, P);
   const int32_t nb = ceil_div(N, B);
   const int32_t S = c.text > 0 ? T + 1 : T;   // segments: frames, then text
-  thread_local std::vector<int32_t> lo, hi;
-  thread_local std::vector<uint8_t> anchor;
-  lo.resize(T);
-  hi.resize(T);
-  anchor.resize(T);
+  HostScratch& hs = host_scratch();
+  hs.lo.resize(T);
+  hs.hi.resize(T);
+  hs.anchor.resize(T);
+  int32_t* const lo = hs.lo.data();
+  int32_t* const hi = hs.hi.data();
+  uint8_t* const anchor = hs.anchor.data();
   for (int32_t t = 0; t < T; ++t) {
     anchor[t] = is_anchor(c, t) ? 1 : 0;
     frame_window(c, t, &lo[t], &hi[t]);
@@ -54,40 +79,42 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
   };
   // Per key block: its frames and split point, so an entry word costs four
   // table lookups.
-  thread_local std::vector<int32_t> kg0, kg1;
-  thread_local std::vector<uint32_t> kfirst;
   if (entry) {
-    kg0.resize(nb);
-    kg1.resize(nb);
-    kfirst.resize(nb);
+    hs.kg0.resize(nb);
+    hs.kg1.resize(nb);
+    hs.kfirst.resize(nb);
     for (int32_t b = 0; b < nb; ++b)
-      key_block_split(b, T, P, B, N, &kg0[b], &kg1[b], &kfirst[b]);
+      key_block_split(b, T, P, B, N, &hs.kg0[b], &hs.kg1[b], &hs.kfirst[b]);
   }
+  const int32_t* const kg0 = hs.kg0.data();
+  const int32_t* const kg1 = hs.kg1.data();
+  const uint32_t* const kfirst = hs.kfirst.data();
 
   // Pass 1: the distinct rows (one per run of query blocks touching the same
-  // frames) into small scratch arrays, and every row's length.
-  thread_local std::vector<int32_t> uniq;
-  thread_local std::vector<uint32_t> uniq_e;
-  thread_local std::vector<int64_t> src;
-  thread_local std::vector<uint8_t> attended;
-  uniq.clear();
-  uniq_e.clear();
-  src.resize(nb);
-  attended.resize(S);
+  // frames) into the working arrays, and every row's length.
+  hs.src.resize(nb);
+  hs.attended.resize(S);
+  int64_t* const src = hs.src.data();
+  uint8_t* const attended = hs.attended.data();
   row_ptr->assign(nb + 1, 0);
+  int32_t* const rp = row_ptr->data();
+  size_t used = 0;
   int32_t prev_first = -1, prev_last = -1;
   int64_t prev_begin = 0, prev_len = 0;
   for (int32_t qb = 0; qb < nb; ++qb) {
     int32_t f0, f1;
     block_frame_range(qb, T, P, B, N, &f0, &f1);
     if (f0 != prev_first || f1 != prev_last) {
-      prev_begin = (int64_t)uniq.size();
+      ensure(hs.uniq, used, nb);
+      if (entry) ensure(hs.uniq_e, used, nb);
+      int32_t* const u = hs.uniq.data();
+      uint32_t* const ue = hs.uniq_e.data();
+      prev_begin = (int64_t)used;
       if (f1 == T) {
-        std::fill(attended.begin(), attended.end(), 1);   // text queries: all
+        std::memset(attended, 1, S);                      // text queries: all
       } else {
-        std::memcpy(attended.data(), anchor.data(), T);
-        for (int32_t t = f0; t <= f1; ++t)
-          std::fill(attended.begin() + lo[t], attended.begin() + hi[t] + 1, 1);
+        std::memcpy(attended, anchor, T);
+        for (int32_t t = f0; t <= f1; ++t) std::memset(attended + lo[t], 1, hi[t] - lo[t] + 1);
         if (S > T) attended[T] = 1;                       // text keys: all
       }
       int32_t last = -1;
@@ -95,36 +122,38 @@ void build_csr_host(const FrameCfg& c, int32_t P, int32_t B,
         if (!attended[tau]) continue;
         int32_t b0, b1;
         segment_blocks(tau, T, P, B, N, &b0, &b1);
-        for (int32_t b = std::max(b0, last + 1); b <= b1; ++b) uniq.push_back(b);
+        const int32_t from = std::max(b0, last + 1);
         if (entry) {
           // A block inside segment tau has the same word as its neighbours
           // but for kb: the 2x2 pattern collapses to tau's two rows.
           const uint32_t q0 = attends(f0, tau) ? 3u : 0u, q1 = attends(f1, tau) ? 12u : 0u;
           const uint32_t inner = ((uint32_t)B << 16) | ((q0 | q1) << 24);
-          for (int32_t b = std::max(b0, last + 1); b <= b1; ++b)
-            uniq_e.push_back(kg0[b] == kg1[b]
-                                 ? (uint32_t)b | inner
-                                 : exact_word(b, kg0[b], kg1[b], kfirst[b], f0, f1, attends));
+          for (int32_t b = from; b <= b1; ++b)
+            ue[used + (b - from)] = kg0[b] == kg1[b]
+                                        ? (uint32_t)b | inner
+                                        : exact_word(b, kg0[b], kg1[b], kfirst[b], f0, f1, attends);
         }
+        for (int32_t b = from; b <= b1; ++b) u[used++] = b;
         last = std::max(last, b1);
       }
-      prev_len = (int64_t)uniq.size() - prev_begin;
+      prev_len = (int64_t)used - prev_begin;
       prev_first = f0;
       prev_last = f1;
     }
     src[qb] = prev_begin;
-    (*row_ptr)[qb + 1] = (*row_ptr)[qb] + (int32_t)prev_len;
+    rp[qb + 1] = rp[qb] + (int32_t)prev_len;
   }
 
   // Pass 2: one allocation of the final size, rows copied in.
-  const int64_t nnz = (*row_ptr)[nb];
+  const int64_t nnz = rp[nb];
   col_idx->resize(nnz);
   if (entry) entry->resize(nnz);
+  const int32_t* const u = hs.uniq.data();
+  const uint32_t* const ue = hs.uniq_e.data();
   for (int32_t qb = 0; qb < nb; ++qb) {
-    const int64_t dst = (*row_ptr)[qb], len = (*row_ptr)[qb + 1] - dst;
-    std::memcpy(col_idx->data() + dst, uniq.data() + src[qb], len * sizeof(int32_t));
-    if (entry)
-      std::memcpy(entry->data() + dst, uniq_e.data() + src[qb], len * sizeof(uint32_t));
+    const int64_t dst = rp[qb], len = rp[qb + 1] - dst;
+    std::memcpy(col_idx->data() + dst, u + src[qb], len * sizeof(int32_t));
+    if (entry) std::memcpy(entry->data() + dst, ue + src[qb], len * sizeof(uint32_t));
   }
 }
 
