@@ -19,6 +19,7 @@ oracle on a bounded sample.
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -82,17 +83,27 @@ def percentile(xs, q):
     return xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]
 
 
+def kernel_code_hash(path=ATTN_SRC):
+    """sha256 of the kernel source's code: comments removed and whitespace
+    collapsed, so that a change to the comments alone keeps the hash and any
+    change to the code does not."""
+    text = open(path, encoding="utf-8").read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = " ".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()
+
+
 def traffic_from_profile(workload, kernel):
     """HBM bytes per launch of `kernel` at `workload` from the committed PMC
     summary of that workload (profiles/attn_pmc_<workload>.json), if it was taken
-    on the current kernel source; else None."""
+    on the current kernel code; else None."""
     path = os.path.join(PROFILES, f"attn_pmc_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    src = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
-    if rec.get("attention_src_sha256") != src or rec.get("workload") != workload:
+    if rec.get("attention_code_sha256") != kernel_code_hash() or rec.get("workload") != workload:
         return None
     k = rec.get("kernels", {}).get(kernel)
     return None if k is None else k.get("hbm_bytes_per_launch")

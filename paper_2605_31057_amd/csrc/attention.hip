@@ -24,26 +24,28 @@
 //   entries of the other row above it (a binary search) minus the entries
 //   above it that both rows hold (a ballot count), and the step words are
 //   written there.  The step loop then reads one word per step, three steps
-//   ahead (K tiles are loaded two steps ahead).  Rows longer than WALK_CAP
-//   are merged WALK_CAP words at a time between steps.  The mask is only
-//   read, so any number of launches can share it.
+//   ahead (K tiles are loaded two steps ahead).  The sparse modes take at most
+//   WALK_CAP key blocks (checked before launch), so one merge covers any
+//   pair.  Dense attention up to WALK_CAP key blocks runs the block mode with
+//   no CSR: the words are written directly instead of merged.  The mask is
+//   only read, so any number of launches can share it.
 //
 // Schedule ("ping-pong", one key block per step)
 //   Waves w and w + NW/2 (which share a SIMD when NW = 8) run half a step
-//   apart: while one is in its GEMM phase (O += P(j) V(j), l += row sums of
-//   P(j), S(j+1) = K(j+1) Q^T: MFMA with fragments from LDS) the other is in
-//   its softmax phase (row max, exponentials, P in bf16: VALU), so the matrix
+//   apart: while one is in its GEMM phase (O += P(j) V(j), S(j+1) = K(j+1)
+//   Q^T: MFMA with fragments from LDS) the other is in its softmax phase (row
+//   max, exponentials, P in bf16: VALU), so the matrix
 //   core and the VALU of each SIMD are busy at the same time.  A barrier ends
 //   every half step.  LDS holds two K stages and two V stages (slab layout,
 //   see below); K(j+2) and V(j+1) stream from HBM/L2 into the stages freed by
 //   step j-1 with buffer loads that write LDS directly, issued during the
 //   first half of step j and waited for at its end.  The buffer resource's
 //   size bound turns rows at or past N (ragged last block) into zeros.
-//   Row sums come from the matrix core: in the GEMM phase a 16x16x32 MFMA
+//   Row sums (RowSums): in the block mode, 64 fp32 adds per step in the
+//   softmax phase; in the other modes the matrix core, where a 16x16x32 MFMA
 //   with a constant 0/1 A operand adds up each 16-key step of P for all 32
-//   rows of the wave.  That takes the adds off the softmax phase, for 8 small
-//   MFMAs per step (1/16 of the step's matrix work), and sums exactly the
-//   bf16 P that multiplies V.
+//   rows of the wave in the GEMM phase (8 small MFMAs per step, summing
+//   exactly the bf16 P that multiplies V).
 //   A whole key block per step keeps the per-step costs (two barriers, the
 //   loop, the load set-up) small against the step's 72 MFMAs per wave; S
 //   (64 registers) and P (32) then fill the register file, so the GEMM
